@@ -1,0 +1,199 @@
+/*
+ * aio.h -- C ABI of the batch-1 decode step on MI355X (gfx950).
+ *
+ * The operation.  A-IO (arXiv 2604.09752) routes requests between a 1B probe
+ * and a 7B backbone because batch-1 autoregressive decoding is bound by HBM
+ * bandwidth: every generated token fetches the full weight set (Section 2.1,
+ * "The Memory-Bound Dilemma"; Section 3.1, about 14 GB per token for the 7B
+ * and 2 GB for the 1B).  This library is that decode step for a dense
+ * decoder-only transformer -- pre-norm RMSNorm, rotate-half RoPE,
+ * grouped-query attention, SwiGLU FFN, untied LM head, no biases -- in
+ * hand-written HIP kernels.  It also provides the two variants the paper
+ * toggles per request (Section 3.3 "Strategy Routing", Section 4.2): W8A16
+ * storage-only quantization (int8 weights, fp16 per-output-channel scales,
+ * dequantised inside the matrix-vector kernels) and the one-forward
+ * verification of prompt-lookup drafts.
+ *
+ * Conventions.
+ *  - Every pointer named *_dev is a device pointer on the current HIP device;
+ *    the caller allocates and owns it (weights, KV cache, workspace, logits,
+ *    token buffers).  The library only borrows them, never frees them, and
+ *    keeps using the weight, KV and workspace pointers until aio_model_free.
+ *  - The library owns only the model handle, a RoPE cos/sin table and any
+ *    captured graph; aio_model_free releases exactly those.
+ *  - Weight matrices are row-major [out][in] (y = W x).  bf16 is stored as
+ *    uint16 bit patterns, fp16 scales likewise.
+ *  - Device pointers must be 16-byte aligned (the workspace 256-byte
+ *    aligned); d_model and ffn_dim must be multiples of 64.
+ *  - All calls are asynchronous on the stream given at load time: a return of
+ *    AIO_OK means the work is enqueued.  Results are valid after a stream
+ *    synchronisation; device faults surface there.
+ *  - Every argument is checked on the host before anything is enqueued; a
+ *    rejected call enqueues nothing and changes nothing.  No call aborts or
+ *    exits the process and no C++ exception crosses this interface.
+ *  - A handle is not thread-safe; distinct handles are independent (a 1B and a
+ *    7B model can be resident together, as in the paper's Section 3.1).
+ *  - Decode state is (KV cache contents, position), owned by the caller.  Rows
+ *    of the cache beyond the current position are never read, so rolling back
+ *    after a rejected draft is just calling again at the earlier position.
+ */
+#ifndef AIO_H
+#define AIO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- errors */
+enum {
+  AIO_OK = 0,
+  AIO_EINVAL = -1,       /* null or misaligned pointer, inconsistent config */
+  AIO_ERANGE = -2,       /* token or position out of range, k out of range  */
+  AIO_EUNSUPPORTED = -3, /* shape or device this build does not handle      */
+  AIO_EHIP = -4,         /* a HIP runtime or launch error; see aio_last_hip_error */
+  AIO_ENOMEM = -5        /* the library's own small allocations failed      */
+};
+
+/* Weight storage formats. */
+enum {
+  AIO_WFMT_BF16 = 0, /* every projection and the LM head in bf16            */
+  AIO_WFMT_INT8 = 1  /* W8A16: int8 [out][in] + fp16 scale [out], symmetric,
+                        no zero point, W[n,k] = q[n,k] * s[n]; embedding and
+                        norm gains stay bf16                                 */
+};
+
+/* Largest number of rows (the current token plus drafts) one aio_verify call
+ * scores. */
+#define AIO_MAX_VERIFY_ROWS 10
+
+typedef struct aio_config {
+  int32_t n_layers;   /* L                                                  */
+  int32_t d_model;    /* d, multiple of 64                                  */
+  int32_t n_heads;    /* H query heads                                      */
+  int32_t n_kv_heads; /* Hkv key/value heads, H % Hkv == 0                  */
+  int32_t head_dim;   /* hd, 64 or 128                                      */
+  int32_t ffn_dim;    /* F, multiple of 64                                  */
+  int32_t vocab;      /* V                                                  */
+  int32_t max_ctx;    /* positions the KV cache holds                       */
+  int32_t max_verify; /* rows per aio_verify call, 1..AIO_MAX_VERIFY_ROWS   */
+  int32_t wfmt;       /* AIO_WFMT_BF16 or AIO_WFMT_INT8                     */
+  float rms_eps;      /* RMSNorm epsilon (inside the square root)           */
+  float rope_base;    /* RoPE base; theta_i = base^(-2i/hd)                 */
+} aio_config;
+
+/* Per-layer weights (device pointers).  Norm gains are bf16 [d].  With
+ * AIO_WFMT_BF16 the projections are bf16 and the s_* scales must be NULL; with
+ * AIO_WFMT_INT8 they are int8 and every s_* is an fp16 [out] array. */
+typedef struct aio_layer_weights {
+  const void* attn_norm; /* [d]                  */
+  const void* ffn_norm;  /* [d]                  */
+  const void* wq;        /* [H*hd][d]            */
+  const void* wk;        /* [Hkv*hd][d]          */
+  const void* wv;        /* [Hkv*hd][d]          */
+  const void* wo;        /* [d][H*hd]            */
+  const void* w_gate;    /* [F][d]               */
+  const void* w_up;      /* [F][d]               */
+  const void* w_down;    /* [d][F]               */
+  const void *sq, *sk, *sv, *so, *s_gate, *s_up, *s_down;
+} aio_layer_weights;
+
+typedef struct aio_weights {
+  const void* embed;               /* bf16 [V][d]                             */
+  const void* final_norm;          /* bf16 [d]                                */
+  const void* lm_head;             /* bf16 or int8 [V][d] (untied)            */
+  const void* s_lm_head;           /* fp16 [V] for int8, else NULL            */
+  const aio_layer_weights* layers; /* HOST array of n_layers entries; copied   */
+} aio_weights;
+
+typedef struct aio_model aio_model;
+
+/* ----------------------------------------------------------- pure host calls */
+
+/* Bytes of the KV cache: bf16 [n_layers][2 (K, V)][n_kv_heads][max_ctx][head_dim].
+ * Returns 0 for an invalid config. */
+size_t aio_kv_bytes(const aio_config* cfg);
+
+/* Bytes of device workspace the model needs (activations, split-KV partials,
+ * a small state block).  Returns 0 for an invalid config. */
+size_t aio_workspace_bytes(const aio_config* cfg);
+
+/* AIO_OK, or the error aio_model_load would return for this config. */
+int aio_check_config(const aio_config* cfg);
+
+/* Checks of one call's scalar arguments against a config, exactly as the entry
+ * points make them (AIO_OK, AIO_EINVAL or AIO_ERANGE). */
+int aio_check_decode(const aio_config* cfg, int32_t token, int32_t pos);
+int aio_check_verify(const aio_config* cfg, int32_t token, const int32_t* drafts, int32_t k,
+                     int32_t pos);
+
+const char* aio_strerror(int code);
+
+/* The last hipError_t this library saw on the calling thread (0 if none). */
+int aio_last_hip_error(void);
+
+/* ---------------------------------------------------------- model lifecycle */
+
+/* Binds a model to caller-owned device memory.
+ *  cfg, w      host structs; copied.
+ *  kv_dev      aio_kv_bytes(cfg) bytes; positions the caller has not written
+ *              are never read before a decode or verify call writes them.
+ *  ws_dev      aio_workspace_bytes(cfg) bytes, used only by this handle.
+ *  hip_stream  hipStream_t every later call enqueues on (NULL = default stream).
+ *  out         receives the handle.
+ * Allocates and fills the RoPE table (fp32 cos/sin of angles computed in
+ * double on the host), so it synchronises once.  Fails with AIO_EUNSUPPORTED
+ * on a device that is not gfx950. */
+int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, void* ws_dev,
+                   void* hip_stream, aio_model** out);
+
+void aio_model_free(aio_model* m);
+
+/* ------------------------------------------------------------- the hot path */
+
+/* One decode step (Section 2.1, Section 3.1): consume `token` at position
+ * `pos` (0-based; the cache must hold positions 0..pos-1), write its K and V
+ * at `pos` in every layer, attend over positions [0, pos], and write fp32
+ * logits [vocab] to logits_dev.
+ * AIO_ERANGE: token not in [0, vocab) or pos not in [0, max_ctx). */
+int aio_decode_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev);
+
+/* Prompt-lookup verification in one forward (Section 3.3, Section 4.2): rows
+ * are [token, drafts[0..k-1]] (drafts is a HOST array) at positions
+ * pos..pos+k.  Writes K/V of all k+1 rows; row i of logits_dev (fp32
+ * [k+1][vocab]) equals the logits of aio_decode_step on row i's token after
+ * rows 0..i-1, i.e. row i attends over positions [0, pos+i].
+ * AIO_ERANGE: k < 0, k+1 > max_verify, pos < 0, pos+k >= max_ctx, or a token
+ * outside [0, vocab). */
+int aio_verify(aio_model* m, int32_t token, const int32_t* drafts, int32_t k, int32_t pos,
+               float* logits_dev);
+
+/* Greedy argmax of `rows` rows of `n` fp32 values each (row-major), one
+ * int32 index per row into out_dev.  The lowest index wins ties; NaN ranks
+ * above +Inf (the first NaN wins).  rows in [1, max_verify], n in [1, 2^30]. */
+int aio_argmax(aio_model* m, const float* logits_dev, int32_t rows, int32_t n, int32_t* out_dev);
+
+/* Device-resident greedy decoding for timing: consume `token` at `pos`, then
+ * feed each step's argmax as the next token, for n_steps steps, with no host
+ * round trip inside the loop (the step is replayed from a captured HIP graph
+ * when AIO_GRAPH is not "0").  tokens_dev (int32 [n_steps]) receives the
+ * argmax of every step; logits_dev (fp32 [vocab]) holds the last step's
+ * logits.  AIO_ERANGE if pos + n_steps > max_ctx. */
+int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
+                      int32_t* tokens_dev, float* logits_dev);
+
+/* Profiling: one aio_decode_step with a HIP event recorded on the model's
+ * stream before the first kernel and after every kernel, then a wait for the
+ * last event.  kernel_ms (host, max_kernels floats) receives each kernel's
+ * event-to-event time in launch order -- per layer: qkv, attention,
+ * split merge, o-projection, gate/up, down; then the LM head -- and
+ * *n_kernels the count written.  Synchronises; not for the timed loop. */
+int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
+                     float* kernel_ms, int32_t max_kernels, int32_t* n_kernels);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AIO_H */

@@ -1,0 +1,87 @@
+// Internal structures shared by the host side (api.cpp) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "aio.h"
+
+// Device-resident decode state: the token(s) and position the next kernels
+// consume.  aio_decode_step writes it with a one-thread kernel; in greedy mode
+// the argmax kernel advances it, so a captured step graph can be replayed.
+struct aio_state {
+  int32_t token[16];
+  int32_t pos;
+  int32_t step;
+  int32_t rows;
+  int32_t pad[13];
+};
+
+// Offsets (bytes) of the workspace regions; every region is 256-byte aligned.
+struct WsLayout {
+  size_t state;    // aio_state
+  size_t x;        // fp32 [MV][d]            residual stream
+  size_t q;        // fp32 [MV][H*hd]         rotated queries
+  size_t o;        // fp32 [MV][H*hd]         attention output
+  size_t m;        // fp32 [F]                SwiGLU output (decode)
+  size_t part_o;   // fp32 [MV][H][S][hd]     split-KV partial outputs
+  size_t part_ml;  // fp32 [MV][H][S][2]      split-KV (max, sum) in log2 units
+  size_t act;      // bf16 [2][32][KA]        split activations for the verify GEMM
+  size_t amax;     // int32 [MV]              argmax scratch
+  size_t total;
+  int splits;      // S, split-KV partitions per head
+  int ka;          // KA = max(d, H*hd, F)
+};
+
+WsLayout aio_ws_layout(const aio_config& c);
+
+struct aio_model {
+  aio_config cfg;
+  std::vector<aio_layer_weights> layers;
+  const void* embed;
+  const void* final_norm;
+  const void* lm_head;
+  const void* s_lm_head;
+  uint16_t* kv;          // caller-owned cache
+  char* ws;              // caller-owned workspace
+  hipStream_t stream;
+  float2* rope;          // library-owned [max_ctx][hd/2] (cos, sin)
+  WsLayout lay;
+  int num_cus;
+  hipGraphExec_t greedy_exec;  // one decode step reading aio_state, argmax feeding back
+  float* greedy_logits;        // logits pointer baked into greedy_exec
+  int32_t* greedy_tokens;      // token output pointer baked into greedy_exec
+  bool use_graph;
+  // profiling: when prof_ev is set, every launcher records one event after
+  // each kernel it enqueues (aio_profile_step)
+  mutable hipEvent_t* prof_ev;
+  mutable int prof_n;
+  int prof_cap;
+
+  aio_state* state() const { return (aio_state*)(ws + lay.state); }
+  template <class T>
+  T* at(size_t off) const { return (T*)(ws + off); }
+  uint16_t* kv_layer(int l, int kind) const {  // kind 0 = K, 1 = V
+    size_t per = (size_t)cfg.n_kv_heads * (size_t)cfg.max_ctx * (size_t)cfg.head_dim;
+    return kv + ((size_t)l * 2 + (size_t)kind) * per;
+  }
+};
+
+// Records the next profiling event after a kernel launch (no-op unless
+// aio_profile_step is running).
+inline void aio_prof_mark(const aio_model& m) {
+  if (m.prof_ev && m.prof_n < m.prof_cap) (void)hipEventRecord(m.prof_ev[m.prof_n++], m.stream);
+}
+
+// ---- launchers (decode_kernels.hip); each enqueues on m.stream ----
+hipError_t aio_launch_set_state(const aio_model& m, int32_t token, int32_t pos);
+hipError_t aio_launch_set_rows(const aio_model& m, const int32_t* toks, int rows, int32_t pos);
+hipError_t aio_launch_decode_layer(const aio_model& m, int l);
+hipError_t aio_launch_lm_head(const aio_model& m, float* logits);
+hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, int n,
+                             int32_t* out, bool greedy_feedback);
+
+// ---- launchers (verify_kernels.hip) ----
+hipError_t aio_launch_verify(const aio_model& m, int rows, float* logits);

@@ -1,0 +1,352 @@
+// Host side of the C ABI declared in include/aio.h: argument checks, the
+// workspace layout, model load (RoPE table), and launch sequencing.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "aio_internal.h"
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+int hip_fail(hipError_t e) {
+  g_last_hip = (int)e;
+  return AIO_EHIP;
+}
+
+size_t align256(size_t v) { return (v + 255u) & ~(size_t)255u; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int env_int(const char* name, int dflt) {
+  const char* s = getenv(name);
+  if (!s || !*s) return dflt;
+  return atoi(s);
+}
+
+// Split-KV partitions per head: enough (split, kv head) workgroups to cover
+// the 256 CUs about twice, but no split shorter than 64 keys at full context.
+int choose_splits(const aio_config& c) {
+  int s = env_int("AIO_SPLITS", 0);
+  if (s <= 0) {
+    s = (512 + c.n_kv_heads - 1) / c.n_kv_heads;
+    int cap = c.max_ctx / 64;
+    if (cap < 1) cap = 1;
+    if (s > cap) s = cap;
+  }
+  if (s > 256) s = 256;
+  if (s < 1) s = 1;
+  return s;
+}
+
+}  // namespace
+
+WsLayout aio_ws_layout(const aio_config& c) {
+  WsLayout L{};
+  const size_t MV = (size_t)c.max_verify, d = (size_t)c.d_model, F = (size_t)c.ffn_dim;
+  const size_t Hd = (size_t)c.n_heads * (size_t)c.head_dim;
+  L.splits = choose_splits(c);
+  size_t ka = d > Hd ? d : Hd;
+  if (F > ka) ka = F;
+  L.ka = (int)ka;
+  size_t off = 0;
+  L.state = off; off = align256(off + sizeof(aio_state));
+  L.x = off; off = align256(off + MV * d * 4);
+  L.q = off; off = align256(off + MV * Hd * 4);
+  L.o = off; off = align256(off + MV * Hd * 4);
+  L.m = off; off = align256(off + F * 4);
+  L.part_o = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * c.head_dim * 4);
+  L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * 2 * 4);
+  L.act = off; off = align256(off + 2 * 32 * ka * 2);  // two split-activation buffers
+  L.amax = off; off = align256(off + MV * 4);
+  L.total = off;
+  return L;
+}
+
+extern "C" {
+
+int aio_check_config(const aio_config* c) {
+  if (!c) return AIO_EINVAL;
+  if (c->n_layers < 1 || c->d_model < 64 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+      c->ffn_dim < 64 || c->vocab < 1 || c->max_ctx < 1 || c->head_dim < 1)
+    return AIO_EINVAL;
+  if (c->n_heads % c->n_kv_heads) return AIO_EINVAL;
+  if (c->d_model % 64 || c->ffn_dim % 64) return AIO_EINVAL;
+  if (c->wfmt != AIO_WFMT_BF16 && c->wfmt != AIO_WFMT_INT8) return AIO_EINVAL;
+  if (!(c->rms_eps > 0.f) || !isfinite(c->rms_eps)) return AIO_EINVAL;
+  if (!(c->rope_base > 1.f) || !isfinite(c->rope_base)) return AIO_EINVAL;
+  if (c->max_verify < 1 || c->max_verify > AIO_MAX_VERIFY_ROWS) return AIO_EINVAL;
+  if (c->head_dim != 64 && c->head_dim != 128) return AIO_EUNSUPPORTED;
+  const int G = c->n_heads / c->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return AIO_EUNSUPPORTED;
+  if (c->max_ctx > (1 << 24) || c->vocab > (1 << 24) || c->d_model > (1 << 16) ||
+      c->ffn_dim > (1 << 16) || c->n_layers > 1024 || c->n_heads > 1024)
+    return AIO_EUNSUPPORTED;
+  if ((size_t)c->n_heads * c->head_dim > 65536) return AIO_EUNSUPPORTED;
+  return AIO_OK;
+}
+
+size_t aio_kv_bytes(const aio_config* c) {
+  if (aio_check_config(c) != AIO_OK) return 0;
+  return (size_t)c->n_layers * 2 * (size_t)c->n_kv_heads * (size_t)c->max_ctx *
+         (size_t)c->head_dim * 2;
+}
+
+size_t aio_workspace_bytes(const aio_config* c) {
+  if (aio_check_config(c) != AIO_OK) return 0;
+  return aio_ws_layout(*c).total;
+}
+
+int aio_check_decode(const aio_config* c, int32_t token, int32_t pos) {
+  int rc = aio_check_config(c);
+  if (rc) return rc;
+  if (token < 0 || token >= c->vocab) return AIO_ERANGE;
+  if (pos < 0 || pos >= c->max_ctx) return AIO_ERANGE;
+  return AIO_OK;
+}
+
+int aio_check_verify(const aio_config* c, int32_t token, const int32_t* drafts, int32_t k,
+                     int32_t pos) {
+  int rc = aio_check_config(c);
+  if (rc) return rc;
+  if (k < 0 || k + 1 > c->max_verify) return AIO_ERANGE;
+  if (k > 0 && !drafts) return AIO_EINVAL;
+  if (pos < 0 || (int64_t)pos + k >= (int64_t)c->max_ctx) return AIO_ERANGE;
+  if (token < 0 || token >= c->vocab) return AIO_ERANGE;
+  for (int i = 0; i < k; ++i)
+    if (drafts[i] < 0 || drafts[i] >= c->vocab) return AIO_ERANGE;
+  return AIO_OK;
+}
+
+const char* aio_strerror(int code) {
+  switch (code) {
+    case AIO_OK: return "ok";
+    case AIO_EINVAL: return "invalid argument (null or misaligned pointer, inconsistent config)";
+    case AIO_ERANGE: return "argument out of range (token, position or draft count)";
+    case AIO_EUNSUPPORTED: return "unsupported shape or device";
+    case AIO_EHIP: return "HIP runtime error";
+    case AIO_ENOMEM: return "out of host or device memory";
+    default: return "unknown error";
+  }
+}
+
+int aio_last_hip_error(void) { return g_last_hip; }
+
+static int check_weights(const aio_config& c, const aio_weights* w) {
+  if (!w || !w->layers) return AIO_EINVAL;
+  const bool int8 = c.wfmt == AIO_WFMT_INT8;
+  auto need = [](const void* p) { return p && aligned16(p); };
+  auto scale_ok = [&](const void* s) { return int8 ? need(s) : s == nullptr; };
+  if (!need(w->embed) || !need(w->final_norm) || !need(w->lm_head) || !scale_ok(w->s_lm_head))
+    return AIO_EINVAL;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const aio_layer_weights& L = w->layers[l];
+    const void* mats[] = {L.wq, L.wk, L.wv, L.wo, L.w_gate, L.w_up, L.w_down};
+    const void* scs[] = {L.sq, L.sk, L.sv, L.so, L.s_gate, L.s_up, L.s_down};
+    if (!need(L.attn_norm) || !need(L.ffn_norm)) return AIO_EINVAL;
+    for (int i = 0; i < 7; ++i)
+      if (!need(mats[i]) || !scale_ok(scs[i])) return AIO_EINVAL;
+  }
+  return AIO_OK;
+}
+
+int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, void* ws_dev,
+                   void* hip_stream, aio_model** out) {
+  if (!out) return AIO_EINVAL;
+  *out = nullptr;
+  int rc = aio_check_config(cfg);
+  if (rc) return rc;
+  if ((rc = check_weights(*cfg, w))) return rc;
+  if (!kv_dev || !ws_dev || !aligned16(kv_dev) || ((uintptr_t)ws_dev & 255u)) return AIO_EINVAL;
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  hipDeviceProp_t prop;
+  if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return hip_fail(e);
+  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return AIO_EUNSUPPORTED;
+
+  aio_model* m = new (std::nothrow) aio_model();
+  if (!m) return AIO_ENOMEM;
+  m->cfg = *cfg;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  m->s_lm_head = w->s_lm_head;
+  m->kv = (uint16_t*)kv_dev;
+  m->ws = (char*)ws_dev;
+  m->stream = (hipStream_t)hip_stream;
+  m->lay = aio_ws_layout(*cfg);
+  m->num_cus = prop.multiProcessorCount;
+  m->greedy_exec = nullptr;
+  m->greedy_logits = nullptr;
+  m->greedy_tokens = nullptr;
+  const char* g = getenv("AIO_GRAPH");
+  m->use_graph = !(g && strcmp(g, "0") == 0) && hip_stream != nullptr;
+
+  // RoPE table: cos/sin of pos * base^(-2i/hd), angles in double, stored fp32.
+  const int half = cfg->head_dim / 2;
+  const size_t n = (size_t)cfg->max_ctx * (size_t)half;
+  float2* host = (float2*)malloc(n * sizeof(float2));
+  if (!host) { delete m; return AIO_ENOMEM; }
+  for (int i = 0; i < half; ++i) {
+    const double theta = pow((double)cfg->rope_base, -2.0 * (double)i / (double)cfg->head_dim);
+    for (int p = 0; p < cfg->max_ctx; ++p) {
+      const double phi = (double)p * theta;
+      host[(size_t)p * half + i] = make_float2((float)cos(phi), (float)sin(phi));
+    }
+  }
+  e = hipMalloc((void**)&m->rope, n * sizeof(float2));
+  if (e == hipSuccess) e = hipMemcpy(m->rope, host, n * sizeof(float2), hipMemcpyHostToDevice);
+  free(host);
+  if (e != hipSuccess) {
+    if (m->rope) (void)hipFree(m->rope);
+    delete m;
+    return hip_fail(e);
+  }
+  *out = m;
+  return AIO_OK;
+}
+
+void aio_model_free(aio_model* m) {
+  if (!m) return;
+  if (m->prof_ev) {
+    for (int i = 0; i < m->prof_cap + 1; ++i) (void)hipEventDestroy(m->prof_ev[i]);
+    free(m->prof_ev);
+  }
+  if (m->greedy_exec) (void)hipGraphExecDestroy(m->greedy_exec);
+  if (m->rope) (void)hipFree(m->rope);
+  delete m;
+}
+
+static hipError_t enqueue_step_body(aio_model* m, float* logits) {
+  hipError_t e;
+  for (int l = 0; l < m->cfg.n_layers; ++l)
+    if ((e = aio_launch_decode_layer(*m, l)) != hipSuccess) return e;
+  return aio_launch_lm_head(*m, logits);
+}
+
+int aio_decode_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev) {
+  if (!m || !logits_dev || !aligned16(logits_dev)) return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  hipError_t e = aio_launch_set_state(*m, token, pos);
+  if (e == hipSuccess) e = enqueue_step_body(m, logits_dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
+}
+
+int aio_verify(aio_model* m, int32_t token, const int32_t* drafts, int32_t k, int32_t pos,
+               float* logits_dev) {
+  if (!m || !logits_dev || !aligned16(logits_dev)) return AIO_EINVAL;
+  int rc = aio_check_verify(&m->cfg, token, drafts, k, pos);
+  if (rc) return rc;
+  int32_t rows[AIO_MAX_VERIFY_ROWS];
+  rows[0] = token;
+  for (int i = 0; i < k; ++i) rows[i + 1] = drafts[i];
+  hipError_t e = aio_launch_set_rows(*m, rows, k + 1, pos);
+  if (e == hipSuccess) e = aio_launch_verify(*m, k + 1, logits_dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
+}
+
+int aio_argmax(aio_model* m, const float* logits_dev, int32_t rows, int32_t n, int32_t* out_dev) {
+  if (!m || !logits_dev || !out_dev) return AIO_EINVAL;
+  if (((uintptr_t)logits_dev & 3u) || ((uintptr_t)out_dev & 3u)) return AIO_EINVAL;
+  if (rows < 1 || rows > 65535 || n < 1 || n > (1 << 30)) return AIO_ERANGE;
+  hipError_t e = aio_launch_argmax(*m, logits_dev, rows, n, out_dev, false);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
+}
+
+static hipError_t enqueue_greedy_body(aio_model* m, float* logits, int32_t* tokens) {
+  hipError_t e = enqueue_step_body(m, logits);
+  if (e != hipSuccess) return e;
+  return aio_launch_argmax(*m, logits, 1, m->cfg.vocab, tokens, true);
+}
+
+static hipError_t ensure_greedy_graph(aio_model* m, float* logits, int32_t* tokens) {
+  if (m->greedy_exec && m->greedy_logits == logits && m->greedy_tokens == tokens)
+    return hipSuccess;
+  if (m->greedy_exec) {
+    (void)hipGraphExecDestroy(m->greedy_exec);
+    m->greedy_exec = nullptr;
+  }
+  hipGraph_t graph = nullptr;
+  hipError_t e = hipStreamBeginCapture(m->stream, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) return e;
+  hipError_t body = enqueue_greedy_body(m, logits, tokens);
+  e = hipStreamEndCapture(m->stream, &graph);
+  if (body != hipSuccess) e = body;
+  if (e == hipSuccess) e = hipGraphInstantiate(&m->greedy_exec, graph, nullptr, nullptr, 0);
+  if (graph) (void)hipGraphDestroy(graph);
+  if (e != hipSuccess) {
+    m->greedy_exec = nullptr;
+    return e;
+  }
+  m->greedy_logits = logits;
+  m->greedy_tokens = tokens;
+  return hipSuccess;
+}
+
+int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
+                      int32_t* tokens_dev, float* logits_dev) {
+  if (!m || !tokens_dev || !logits_dev || !aligned16(logits_dev) || ((uintptr_t)tokens_dev & 3u))
+    return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  if (n_steps < 1 || (int64_t)pos + n_steps > (int64_t)m->cfg.max_ctx) return AIO_ERANGE;
+  hipError_t e = aio_launch_set_state(*m, token, pos);
+  if (e != hipSuccess) return hip_fail(e);
+  if (m->use_graph) {
+    if ((e = ensure_greedy_graph(m, logits_dev, tokens_dev)) != hipSuccess) return hip_fail(e);
+    for (int s = 0; s < n_steps; ++s)
+      if ((e = hipGraphLaunch(m->greedy_exec, m->stream)) != hipSuccess) return hip_fail(e);
+    return AIO_OK;
+  }
+  for (int s = 0; s < n_steps; ++s)
+    if ((e = enqueue_greedy_body(m, logits_dev, tokens_dev)) != hipSuccess) return hip_fail(e);
+  return AIO_OK;
+}
+
+int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
+                     float* kernel_ms, int32_t max_kernels, int32_t* n_kernels) {
+  if (!m || !logits_dev || !aligned16(logits_dev) || !kernel_ms || !n_kernels || max_kernels < 1)
+    return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  const int need = 6 * m->cfg.n_layers + 1;
+  if (!m->prof_ev) {
+    m->prof_ev = (hipEvent_t*)calloc((size_t)need + 1, sizeof(hipEvent_t));
+    if (!m->prof_ev) return AIO_ENOMEM;
+    for (int i = 0; i < need + 1; ++i) {
+      hipError_t e = hipEventCreate(&m->prof_ev[i]);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    m->prof_cap = need;
+  }
+  hipError_t e = aio_launch_set_state(*m, token, pos);
+  if (e == hipSuccess) e = hipEventRecord(m->prof_ev[0], m->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  hipEvent_t* saved = m->prof_ev;
+  m->prof_ev = saved + 1;  // events 1..need follow the kernels
+  m->prof_n = 0;
+  e = enqueue_step_body(m, logits_dev);
+  const int n = m->prof_n;
+  m->prof_ev = saved;
+  m->prof_n = 0;
+  if (e != hipSuccess) return hip_fail(e);
+  if ((e = hipEventSynchronize(saved[n])) != hipSuccess) return hip_fail(e);
+  const int out = n < max_kernels ? n : max_kernels;
+  for (int i = 0; i < out; ++i) {
+    float ms = 0.f;
+    if ((e = hipEventElapsedTime(&ms, saved[i], saved[i + 1])) != hipSuccess) return hip_fail(e);
+    kernel_ms[i] = ms;
+  }
+  *n_kernels = out;
+  return AIO_OK;
+}
+
+}  // extern "C"

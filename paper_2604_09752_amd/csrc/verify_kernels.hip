@@ -1,0 +1,519 @@
+// Verify forward (prompt-lookup verification): M = k + 1 <= 10 rows at
+// positions pos .. pos + k in one pass over the weights, for gfx950.
+//
+// At M rows a projection does ~M flops per weight byte (8-16 flop/B), close
+// to the fp32 VALU ridge, so the matrix products run on MFMA
+// (v_mfma_f32_32x32x16_bf16).  MFMA inputs are bf16; to keep fp32-level
+// accuracy each fp32 activation a is split exactly into three bf16 terms,
+// a = t0 + t1 + t2 + O(2^-27 a) (t0 = bf16(a), t1 = bf16(a - t0),
+// t2 = bf16(a - t0 - t1); each subtraction is exact in fp32), and the three
+// terms of all M rows form the 3M <= 30 columns of one 32-column B operand.
+// Weights are the A operand (32 output channels per tile); int8 weights
+// convert to bf16 exactly (|q| <= 127) and their fp16 scale is applied in the
+// epilogue.
+//
+// Per layer: vnorm (RMSNorm + split) -> QKV GEMM (+RoPE, K/V append) ->
+// vattn (causal split-KV, row r sees positions [0, pos + r]) -> vmerge
+// (+split) -> O GEMM (+residual) -> vnorm -> gate/up GEMM (+SwiGLU, split)
+// -> down GEMM (+residual); then vnorm -> LM head GEMM -> logits [M][V].
+#include <math.h>
+
+#include "aio_internal.h"
+#include "common.h"
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / AIO_WAVE;
+constexpr int kMaxRows = AIO_MAX_VERIFY_ROWS;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
+
+// Exact three-term bf16 split of an fp32 value.
+AIO_DEV void split3(float a, uint16_t& t0, uint16_t& t1, uint16_t& t2) {
+  t0 = f32_to_bf16(a);
+  const float r1 = a - bf16_to_f32(t0);
+  t1 = f32_to_bf16(r1);
+  const float r2 = r1 - bf16_to_f32(t1);
+  t2 = f32_to_bf16(r2);
+}
+
+AIO_DEV void store_split(uint16_t* act, int lda, int M, int r, int col, float v) {
+  uint16_t t0, t1, t2;
+  split3(v, t0, t1, t2);
+  act[(size_t)r * lda + col] = t0;
+  act[(size_t)(M + r) * lda + col] = t1;
+  act[(size_t)(2 * M + r) * lda + col] = t2;
+}
+
+// ------------------------------------------------------------ RMSNorm rows
+
+struct VNormArgs {
+  const float* x;           // [M][d] residual rows
+  const uint16_t* embed;    // layer 0: embedding table (tokens from state), else null
+  float* x_copy;            // layer 0: x rows written from the embedding
+  const uint16_t* gain;
+  uint16_t* act;            // [32][lda] split output
+  int lda, d, M;
+  const aio_state* st;
+  float eps;
+};
+
+// One workgroup per row r: h = x_r / sqrt(mean(x_r^2) + eps) * g, split.
+__global__ __launch_bounds__(kBlock) void k_vnorm(VNormArgs a) {
+  __shared__ float red[kWaves];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const uint16_t* emb = a.embed ? a.embed + (size_t)a.st->token[r] * a.d : nullptr;
+  const float* xr = a.x + (size_t)r * a.d;
+  float ss = 0.f;
+  for (int e = tid; e < a.d; e += kBlock) {
+    const float v = emb ? bf16_to_f32(emb[e]) : xr[e];
+    ss = fmaf(v, v, ss);
+  }
+  ss = wave_sum(ss);
+  if ((tid & (AIO_WAVE - 1)) == 0) red[tid / AIO_WAVE] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = rsqrtf(tot / (float)a.d + a.eps);
+  for (int e = tid; e < a.d; e += kBlock) {
+    const float v = emb ? bf16_to_f32(emb[e]) : xr[e];
+    if (emb) a.x_copy[(size_t)r * a.d + e] = v;
+    store_split(a.act, a.lda, a.M, r, e, v * inv * bf16_to_f32(a.gain[e]));
+  }
+}
+
+// ------------------------------------------------------------- skinny GEMM
+
+struct VGemmArgs {
+  const uint16_t* act;      // [32][lda] bf16, columns j = term * M + row
+  int lda;
+  const void* w0;           // QKV: wq | SWIGLU: w_gate | else the matrix
+  const void* w1;           // QKV: wk | SWIGLU: w_up
+  const void* w2;           // QKV: wv
+  const uint16_t* s0;
+  const uint16_t* s1;
+  const uint16_t* s2;
+  int N, K, M;
+  float* out;               // QKV: q [M][H*hd] | RESID: x [M][N] | STORE: logits [M][N]
+  int ldo;
+  uint16_t* act_out;        // SWIGLU: split m [32][lda_out]
+  int lda_out;
+  uint16_t* kc;
+  uint16_t* vc;
+  const float2* rope;
+  const aio_state* st;
+  int H, Hkv, hd, max_ctx;
+};
+
+// 16 consecutive k of one weight row as two bf16x8 MFMA fragments.
+template <int WFMT>
+AIO_DEV void load_a(const char* row, int k, bf16x8& lo, bf16x8& hi) {
+  if constexpr (WFMT == AIO_WFMT_BF16) {
+    const uint4* p = (const uint4*)(row + (size_t)k * 2);
+    const uint4 u0 = ld_stream(p), u1 = ld_stream(p + 1);
+    lo = __builtin_bit_cast(bf16x8, u0);
+    hi = __builtin_bit_cast(bf16x8, u1);
+  } else {
+    const uint4 u = ld_stream((const uint4*)(row + k));
+    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    uint32_t o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      // two int8 -> two bf16 (exact: |q| <= 127 has <= 7 significant bits)
+      const uint32_t src = w[i / 2];
+      const int sh = (i & 1) * 16;
+      const float f0 = (float)(int8_t)(src >> sh);
+      const float f1 = (float)(int8_t)(src >> (sh + 8));
+      o[i] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xffff0000u);
+    }
+    lo = __builtin_bit_cast(bf16x8, make_uint4(o[0], o[1], o[2], o[3]));
+    hi = __builtin_bit_cast(bf16x8, make_uint4(o[4], o[5], o[6], o[7]));
+  }
+}
+
+// Each workgroup owns T = 2 tiles of 32 output channels; its 4 waves split
+// K into quarters and their partial 32x32 tiles are summed in LDS.  Lane l
+// of a wave covers weight row (l % 32) of each tile and, in a block of 32 k,
+// the 16 consecutive k starting at 16 * (l / 32); MFMA "a" takes the first 8
+// and MFMA "b" the next 8, and the B operand (activation column l % 32) is
+// loaded with the same k mapping, so the k permutation cancels.
+template <int WFMT, int EPI>
+__global__ __launch_bounds__(kBlock) void k_vgemm(VGemmArgs a) {
+  constexpr int T = 2;
+  __shared__ float red[kWaves][T][32][33];
+  const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
+  const int rl = lane & 31, kh = lane >> 5;
+  const size_t wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
+
+  // tile rows: QKV pairs (rows, rows + hd/2) of one head section, SWIGLU the
+  // same rows of gate and up, otherwise two consecutive tiles.
+  int tile_row[T];
+  const void* tile_w[T];
+  if constexpr (EPI == EPI_QKV) {
+    const int per_head = a.hd / 64;  // tile pairs per head (hd/2 rows / 32)
+    const int head = blockIdx.x / per_head, sub = blockIdx.x % per_head;
+    const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+    int n0 = head * a.hd + sub * 32;
+    const void* w = a.w0;
+    if (n0 >= qrows + krows) { w = a.w2; n0 -= qrows + krows; }
+    else if (n0 >= qrows) { w = a.w1; n0 -= qrows; }
+    tile_row[0] = n0;
+    tile_row[1] = n0 + a.hd / 2;
+    tile_w[0] = tile_w[1] = w;
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    tile_row[0] = tile_row[1] = blockIdx.x * 32;
+    tile_w[0] = a.w0;
+    tile_w[1] = a.w1;
+  } else {
+    tile_row[0] = blockIdx.x * 64;
+    tile_row[1] = blockIdx.x * 64 + 32;
+    tile_w[0] = tile_w[1] = a.w0;
+  }
+  const int n_rows_w = (EPI == EPI_QKV) ? 0 : a.N;  // clamp bound for plain tiles
+  const char* rowp[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    int n = tile_row[t] + rl;
+    if (n_rows_w && n >= n_rows_w) n = n_rows_w - 1;
+    rowp[t] = (const char*)tile_w[t] + (size_t)n * a.K * wbytes;
+  }
+  const bool col_live = rl < 3 * a.M;
+  const uint16_t* actp = a.act + (size_t)rl * a.lda;
+
+  const int nkb = a.K / 32;
+  const int kb0 = wid * nkb / kWaves, kb1 = (wid + 1) * nkb / kWaves;
+  f32x16 acc[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
+
+  for (int kb = kb0; kb < kb1; ++kb) {
+    const int k = kb * 32 + kh * 16;
+    bf16x8 wa[T], wb[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) load_a<WFMT>(rowp[t], k, wa[t], wb[t]);
+    bf16x8 ba, bb;
+    if (col_live) {
+      const uint4* ap = (const uint4*)(actp + k);
+      ba = __builtin_bit_cast(bf16x8, ap[0]);
+      bb = __builtin_bit_cast(bf16x8, ap[1]);
+    } else {
+      ba = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+      bb = ba;
+    }
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[t], ba, acc[t], 0, 0, 0);
+      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[t], bb, acc[t], 0, 0, 0);
+    }
+  }
+  // D layout: lane l, register v -> column j = l % 32,
+  // row i = 8 * (v / 4) + 4 * (l / 32) + (v % 4).
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[wid][t][8 * (v / 4) + 4 * kh + (v % 4)][rl] = acc[t][v];
+  __syncthreads();
+
+  // Sum the four K quarters and the three split terms: y[r][i] for the tile.
+  const int M = a.M;
+  const int pos = a.st->pos;
+  for (int e = tid; e < 32 * M; e += kBlock) {
+    const int i = e % 32, r = e / 32;
+    float y[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w)
+        s += red[w][t][i][r] + red[w][t][i][M + r] + red[w][t][i][2 * M + r];
+      y[t] = s;
+    }
+    if constexpr (EPI == EPI_QKV) {
+      const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+      const int per_head = a.hd / 64;
+      const int head = blockIdx.x / per_head, sub = blockIdx.x % per_head;
+      const int ii = sub * 32 + i;  // index within the first half of the head
+      const int n_lo = head * a.hd + ii;
+      const int half = a.hd / 2;
+      float lo = y[0], hi = y[1];
+      if constexpr (WFMT == AIO_WFMT_INT8) {
+        // both rows of the pair lie in the same (q, k or v) section
+        const uint16_t* sc = a.s0;
+        int m_lo = n_lo;
+        if (n_lo >= qrows + krows) { sc = a.s2; m_lo -= qrows + krows; }
+        else if (n_lo >= qrows) { sc = a.s1; m_lo -= qrows; }
+        lo *= fp16_to_f32(sc[m_lo]);
+        hi *= fp16_to_f32(sc[m_lo + half]);
+      }
+      const int p = pos + r;
+      if (n_lo < qrows + krows) {
+        const float2 cs = a.rope[(size_t)p * half + ii];
+        const float r0 = lo * cs.x - hi * cs.y;
+        const float r1 = hi * cs.x + lo * cs.y;
+        lo = r0;
+        hi = r1;
+      }
+      if (n_lo < qrows) {
+        a.out[(size_t)r * a.ldo + n_lo] = lo;
+        a.out[(size_t)r * a.ldo + n_lo + half] = hi;
+      } else {
+        const bool is_k = n_lo < qrows + krows;
+        const int g = (n_lo - (is_k ? qrows : qrows + krows)) / a.hd;
+        uint16_t* c = (is_k ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
+        c[ii] = f32_to_bf16(lo);
+        c[ii + half] = f32_to_bf16(hi);
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      const int n = tile_row[0] + i;
+      if (n < a.N) {
+        float g = y[0], u = y[1];
+        if constexpr (WFMT == AIO_WFMT_INT8) {
+          g *= fp16_to_f32(a.s0[n]);
+          u *= fp16_to_f32(a.s1[n]);
+        }
+        store_split(a.act_out, a.lda_out, M, r, n, g / (1.f + expf(-g)) * u);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int n = tile_row[t] + i;
+        if (n >= a.N) continue;
+        float v = y[t];
+        if constexpr (WFMT == AIO_WFMT_INT8) v *= fp16_to_f32(a.s0[n]);
+        if constexpr (EPI == EPI_RESID) a.out[(size_t)r * a.ldo + n] += v;
+        else a.out[(size_t)r * a.ldo + n] = v;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------- causal attention
+
+struct VAttnArgs {
+  const float* q;       // [M][H*hd]
+  const uint16_t* kc;   // [Hkv][max_ctx][hd]
+  const uint16_t* vc;
+  float* part_o;        // [M][H][S][hd]
+  float* part_ml;       // [M][H][S][2]
+  const aio_state* st;
+  int H, Hkv, max_ctx, S, M;
+  float scale_log2;
+};
+
+// One workgroup per (split s, query head h).  Keys [0, pos + M - 1] are cut
+// into S splits; row r only takes keys j <= pos + r.
+template <int HD>
+__global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
+  constexpr int LPK = HD / 8, NG = kBlock / LPK;
+  __shared__ float sm_m[NG][kMaxRows], sm_l[NG][kMaxRows];
+  __shared__ float sm_o[NG][HD];
+  const int tid = threadIdx.x, gi = tid / LPK, li = tid % LPK;
+  const int s = blockIdx.x, h = blockIdx.y, G = a.H / a.Hkv, kvh = h / G;
+  const int pos = a.st->pos, M = a.M;
+  const int n_keys = pos + M;
+  const int chunk = (n_keys + a.S - 1) / a.S;
+  const int j0 = s * chunk, j1 = min(n_keys, j0 + chunk);
+  const size_t Hd = (size_t)a.H * HD;
+
+  float q[kMaxRows][8], o[kMaxRows][8], m[kMaxRows], l[kMaxRows];
+#pragma unroll
+  for (int r = 0; r < kMaxRows; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      q[r][i] = r < M ? a.q[r * Hd + (size_t)h * HD + li * 8 + i] * a.scale_log2 : 0.f;
+      o[r][i] = 0.f;
+    }
+  }
+  const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD + li * 8;
+  const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD + li * 8;
+  for (int j = j0 + gi; j < j1; j += NG) {
+    const uint4 kk = *(const uint4*)(kbase + (size_t)j * HD);
+    const uint4 vv = *(const uint4*)(vbase + (size_t)j * HD);
+    const float vf[8] = {bf16_lo(vv.x), bf16_hi(vv.x), bf16_lo(vv.y), bf16_hi(vv.y),
+                         bf16_lo(vv.z), bf16_hi(vv.z), bf16_lo(vv.w), bf16_hi(vv.w)};
+#pragma unroll
+    for (int r = 0; r < kMaxRows; ++r) {
+      if (r < M) {
+        float sc = dot8_bf16(kk, make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
+                             make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f);
+        sc = group_sum<LPK>(sc);
+        if (j <= pos + r) {  // causal: row r sees keys [0, pos + r]
+          const float mn = fmaxf(m[r], sc);
+          const float c = exp2f(m[r] - mn), p = exp2f(sc - mn);
+          l[r] = l[r] * c + p;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) o[r][i] = fmaf(p, vf[i], o[r][i] * c);
+          m[r] = mn;
+        }
+      }
+    }
+  }
+  // combine the NG groups row by row (r is uniform across the block)
+  if (li == 0) {
+#pragma unroll
+    for (int r = 0; r < kMaxRows; ++r) {
+      sm_m[gi][r] = m[r];
+      sm_l[gi][r] = l[r];
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kMaxRows; ++r) {
+    if (r >= M) continue;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sm_o[gi][li * 8 + i] = o[r][i];
+    __syncthreads();
+    for (int dim = tid; dim < HD; dim += kBlock) {
+      float Mx = -INFINITY;
+      for (int k = 0; k < NG; ++k) Mx = fmaxf(Mx, sm_m[k][r]);
+      float L = 0.f, O = 0.f;
+      if (Mx != -INFINITY) {
+        for (int k = 0; k < NG; ++k) {
+          const float mk = sm_m[k][r];
+          if (mk == -INFINITY) continue;
+          const float w = exp2f(mk - Mx);
+          L = fmaf(w, sm_l[k][r], L);
+          O = fmaf(w, sm_o[k][dim], O);
+        }
+      }
+      const size_t slot = ((size_t)r * a.H + h) * a.S + s;
+      a.part_o[slot * HD + dim] = O;
+      if (dim == 0) {
+        a.part_ml[slot * 2] = Mx;
+        a.part_ml[slot * 2 + 1] = L;
+      }
+    }
+  }
+}
+
+struct VMergeArgs {
+  const float* part_o;
+  const float* part_ml;
+  uint16_t* act;  // split o [32][lda]
+  int lda, S, hd, H, M;
+};
+
+__global__ __launch_bounds__(128) void k_vmerge(VMergeArgs a) {
+  const int h = blockIdx.x, r = blockIdx.y;
+  const size_t base = ((size_t)r * a.H + h) * a.S;
+  const float* ml = a.part_ml + base * 2;
+  float Mx = -INFINITY;
+  for (int s = 0; s < a.S; ++s) Mx = fmaxf(Mx, ml[2 * s]);
+  for (int dim = threadIdx.x; dim < a.hd; dim += blockDim.x) {
+    float L = 0.f, O = 0.f;
+    for (int s = 0; s < a.S; ++s) {
+      const float ms = ml[2 * s];
+      if (ms == -INFINITY) continue;
+      const float w = exp2f(ms - Mx);
+      L = fmaf(w, ml[2 * s + 1], L);
+      O = fmaf(w, a.part_o[(base + s) * a.hd + dim], O);
+    }
+    store_split(a.act, a.lda, a.M, r, h * a.hd + dim, O / L);
+  }
+}
+
+template <int EPI>
+hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& a, int blocks) {
+  if (m.cfg.wfmt == AIO_WFMT_INT8)
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), dim3(blocks), dim3(kBlock), 0, m.stream, a);
+  else
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), dim3(blocks), dim3(kBlock), 0, m.stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_vnorm(const aio_model& m, const float* x, const uint16_t* embed, const void* gain,
+                        uint16_t* act, int M) {
+  VNormArgs n{};
+  n.x = x;
+  n.embed = embed;
+  n.x_copy = m.at<float>(m.lay.x);
+  n.gain = (const uint16_t*)gain;
+  n.act = act;
+  n.lda = m.lay.ka;
+  n.d = m.cfg.d_model;
+  n.M = M;
+  n.st = m.state();
+  n.eps = m.cfg.rms_eps;
+  hipLaunchKernelGGL(k_vnorm, dim3(M), dim3(kBlock), 0, m.stream, n);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
+  const aio_config& c = m.cfg;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const int ka = m.lay.ka;
+  // two split-activation buffers: A feeds the QKV / gate-up / LM-head GEMMs,
+  // B feeds the O / down GEMMs.
+  uint16_t* actA = m.at<uint16_t>(m.lay.act);
+  uint16_t* actB = actA + (size_t)32 * ka;
+  float* x = m.at<float>(m.lay.x);
+  float* q = m.at<float>(m.lay.q);
+  hipError_t e;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const aio_layer_weights& L = m.layers[(size_t)l];
+    e = launch_vnorm(m, x, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm, actA, M);
+    if (e != hipSuccess) return e;
+
+    VGemmArgs g{};
+    g.act = actA; g.lda = ka; g.M = M;
+    g.w0 = L.wq; g.w1 = L.wk; g.w2 = L.wv;
+    g.s0 = (const uint16_t*)L.sq; g.s1 = (const uint16_t*)L.sk; g.s2 = (const uint16_t*)L.sv;
+    g.N = (H + 2 * Hkv) * hd; g.K = d;
+    g.out = q; g.ldo = H * hd;
+    g.kc = m.kv_layer(l, 0); g.vc = m.kv_layer(l, 1);
+    g.rope = m.rope; g.st = m.state();
+    g.H = H; g.Hkv = Hkv; g.hd = hd; g.max_ctx = c.max_ctx;
+    if ((e = launch_vgemm<EPI_QKV>(m, g, (H + 2 * Hkv) * (hd / 64))) != hipSuccess) return e;
+
+    VAttnArgs t{};
+    t.q = q; t.kc = g.kc; t.vc = g.vc;
+    t.part_o = m.at<float>(m.lay.part_o);
+    t.part_ml = m.at<float>(m.lay.part_ml);
+    t.st = m.state();
+    t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx; t.S = m.lay.splits; t.M = M;
+    t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
+    if (hd == 128)
+      hipLaunchKernelGGL(k_vattn<128>, dim3(t.S, H), dim3(kBlock), 0, m.stream, t);
+    else
+      hipLaunchKernelGGL(k_vattn<64>, dim3(t.S, H), dim3(kBlock), 0, m.stream, t);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    VMergeArgs mg{t.part_o, t.part_ml, actB, ka, t.S, hd, H, M};
+    hipLaunchKernelGGL(k_vmerge, dim3(H, M), dim3(128), 0, m.stream, mg);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    VGemmArgs o{};
+    o.act = actB; o.lda = ka; o.M = M;
+    o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
+    o.N = d; o.K = H * hd; o.out = x; o.ldo = d; o.st = m.state();
+    if ((e = launch_vgemm<EPI_RESID>(m, o, (d + 63) / 64)) != hipSuccess) return e;
+
+    if ((e = launch_vnorm(m, x, nullptr, L.ffn_norm, actA, M)) != hipSuccess) return e;
+    VGemmArgs gu{};
+    gu.act = actA; gu.lda = ka; gu.M = M;
+    gu.w0 = L.w_gate; gu.w1 = L.w_up;
+    gu.s0 = (const uint16_t*)L.s_gate; gu.s1 = (const uint16_t*)L.s_up;
+    gu.N = F; gu.K = d; gu.act_out = actB; gu.lda_out = ka; gu.st = m.state();
+    if ((e = launch_vgemm<EPI_SWIGLU>(m, gu, (F + 31) / 32)) != hipSuccess) return e;
+
+    VGemmArgs dn{};
+    dn.act = actB; dn.lda = ka; dn.M = M;
+    dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
+    dn.N = d; dn.K = F; dn.out = x; dn.ldo = d; dn.st = m.state();
+    if ((e = launch_vgemm<EPI_RESID>(m, dn, (d + 63) / 64)) != hipSuccess) return e;
+  }
+  if ((e = launch_vnorm(m, x, nullptr, m.final_norm, actA, M)) != hipSuccess) return e;
+  VGemmArgs lm{};
+  lm.act = actA; lm.lda = ka; lm.M = M;
+  lm.w0 = m.lm_head; lm.s0 = (const uint16_t*)m.s_lm_head;
+  lm.N = c.vocab; lm.K = d; lm.out = logits; lm.ldo = c.vocab; lm.st = m.state();
+  return launch_vgemm<EPI_STORE>(m, lm, (c.vocab + 63) / 64);
+}

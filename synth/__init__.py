@@ -145,7 +145,7 @@ class ModelConfig:
     wfmt: str = "bf16"                 # "bf16" or "int8" (per-output-channel fp16 scale)
     prefill_by_model: bool = False
     verify_k: int = 8
-    max_verify: int = 16
+    max_verify: int = 10
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
     weight_std: float = 0.02

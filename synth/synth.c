@@ -98,14 +98,14 @@ static inline uint16_t to_fp16(float f) {
 }
 
 /* Two standard normals from two 32-bit words by the Box-Muller transform,
- * evaluated in double precision: u1 in (0, 1], u2 in [0, 1). */
+ * evaluated in single precision: u1 in (0, 1], u2 in [0, 1). */
 static inline void box_muller(uint32_t a, uint32_t b, double z[2]) {
-  double u1 = ((double)a + 1.0) * (1.0 / 4294967296.0);
-  double u2 = (double)b * (1.0 / 4294967296.0);
-  double r = sqrt(-2.0 * log(u1));
-  double t = 6.283185307179586476925286766559 * u2;
-  z[0] = r * cos(t);
-  z[1] = r * sin(t);
+  float u1 = ((float)(a >> 8) + 1.0f) * (1.0f / 16777216.0f);
+  float u2 = (float)(b >> 8) * (1.0f / 16777216.0f);
+  float r = sqrtf(-2.0f * logf(u1));
+  float t = 6.2831853071795864769f * u2;
+  z[0] = (double)(r * cosf(t));
+  z[1] = (double)(r * sinf(t));
 }
 
 /* out[i] = bf16(mean + std * N(0,1)); elements 4b..4b+3 come from block b. */
