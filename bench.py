@@ -117,23 +117,36 @@ def main() -> int:
         % (args.steps, 1e3 * elapsed / args.steps, 1e3 * gpu_elapsed / args.steps, tps,
            step_bytes / elapsed / 1e9))
 
-    # dominant kernel: the fused gate/up GEMV, timed with events on dm.stream
+    # dominant kernel, timed with HIP events on dm.stream
     L = cfg.n_layers
-    per_kernel = []
-    for r in range(args.profile_steps):
-        per_kernel.append(dm.profile_step(tau0, P, logits))
-    per_kernel = np.stack(per_kernel)  # [iters][6L + 1] ms
-    kinds = {}
-    for i, name in enumerate(KERNELS_PER_LAYER):
-        kinds[name] = float(per_kernel[:, i:6 * L:6].mean() * 1e3)
-    kinds["lm_head"] = float(per_kernel[:, 6 * L].mean() * 1e3)
     wb = 1 if cfg.wfmt == "int8" else 2
-    gu_bytes = 2 * cfg.ffn_dim * cfg.d_model * wb + 2 * cfg.d_model
-    if cfg.wfmt == "int8":
-        gu_bytes += 2 * 2 * cfg.ffn_dim
-    gu_us = kinds["gateup"]
-    achieved = gu_bytes / (gu_us * 1e-6) / 1e9
-    log("per-kernel average us: " + ", ".join("%s %.1f" % kv for kv in kinds.items()))
+    phases = None
+    if dm.uses_step_kernel:
+        # the whole step is one persistent kernel: its bytes are the step's
+        kname = "k_step (whole decode step: all layers + LM head + argmax)"
+        durs = [float(dm.profile_step(tau0, P, logits)[0]) for _ in range(args.profile_steps)]
+        k_us = 1e3 * float(np.mean(durs))
+        k_bytes = traffic.step_bytes(cfg, P)
+        tr = np.stack([dm.trace_step(tau0, P, logits) for _ in range(args.profile_steps)]).mean(0)
+        # between barrier exits: attention, O, gate/up, down, next layer's QKV
+        names = ("attn", "o", "gateup", "down", "qkv")
+        phases = {n: round(float(tr[i::5].mean()), 2) for i, n in enumerate(names)}
+        log("per-phase average us: " + ", ".join("%s %.1f" % kv for kv in phases.items()))
+        kinds = {"k_step": k_us}
+    else:
+        kname = "gate/up GEMV + RMSNorm prologue + SwiGLU epilogue"
+        per_kernel = np.stack([dm.profile_step(tau0, P, logits)
+                               for _ in range(args.profile_steps)])  # [iters][6L + 1] ms
+        kinds = {}
+        for i, name in enumerate(KERNELS_PER_LAYER):
+            kinds[name] = float(per_kernel[:, i:6 * L:6].mean() * 1e3)
+        kinds["lm_head"] = float(per_kernel[:, 6 * L].mean() * 1e3)
+        k_bytes = 2 * cfg.ffn_dim * cfg.d_model * wb + 2 * cfg.d_model
+        if cfg.wfmt == "int8":
+            k_bytes += 2 * 2 * cfg.ffn_dim
+        k_us = kinds["gateup"]
+    achieved = k_bytes / (k_us * 1e-6) / 1e9
+    log("dominant kernel %s: %.1f us per launch, %.0f GB/s" % (kname, k_us, achieved))
 
     result = {
         "metric": METRIC,
@@ -160,16 +173,17 @@ def main() -> int:
         "bytes_per_step": int(step_bytes // args.steps),
         "roofline": {
             "bound": "hbm",
-            "kernel": "gate/up GEMV + RMSNorm prologue + SwiGLU epilogue",
+            "kernel": kname,
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None,
-            "bytes_per_launch": gu_bytes,
-            "avg_launch_us": round(gu_us, 2),
+            "bytes_per_launch": int(k_bytes),
+            "avg_launch_us": round(k_us, 2),
         },
         "kernel_avg_us": {k: round(v, 2) for k, v in kinds.items()},
+        "phase_avg_us": phases,
     }
     if args.config == "7b":
         result["baseline_note"] = ("vs_baseline divides by the paper's 7B FP16 decode TPS at 2K "
@@ -201,7 +215,12 @@ def main() -> int:
         result["greedy_parity"] = {"steps": n_done, "identical_tokens": agree}
         log("oracle: %d steps in %.1fs (%.3f tokens/s, %d threads), greedy ids identical %d/%d"
             % (n_done, c1 - c0, cpu_tps, oracle.num_threads(), agree, n_done))
+    status = dm.status()
     dm.close()
+    if status != 0:
+        print("device status %d: a grid barrier timed out; the run is invalid" % status,
+              file=sys.stderr)
+        return 3
     print(json.dumps(result), flush=True)
     return 0
 

@@ -193,6 +193,25 @@ int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
 int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
                      float* kernel_ms, int32_t max_kernels, int32_t* n_kernels);
 
+/* 1 if this handle runs each decode step as the single persistent kernel
+ * (the default where the shape allows it and AIO_MEGA is not "0"), else 0
+ * (a sequence of per-operation kernels). */
+int aio_uses_step_kernel(const aio_model* m);
+
+/* Phase timing of one decode step of the persistent kernel: the same work as
+ * aio_decode_step, with workgroup 0 recording the device clock as it leaves
+ * each grid barrier.  phase_us (host, max_phases doubles) receives the time
+ * between consecutive barrier exits, i.e. per layer: attention, O
+ * projection, gate/up, down, next layer's QKV; *n_phases the count written.
+ * Synchronises.  AIO_EUNSUPPORTED when the handle does not use that kernel. */
+int aio_trace_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, double* phase_us,
+                   int32_t max_phases, int32_t* n_phases);
+
+/* Synchronises the model's stream and reports the device-side status word:
+ * 0, or 1 if a grid barrier of the persistent kernel gave up waiting (its
+ * results are then invalid).  Synchronises. */
+int aio_device_status(aio_model* m, int32_t* status);
+
 #ifdef __cplusplus
 }
 #endif

@@ -77,6 +77,9 @@ def lib():
         L.aio_argmax.argtypes = [vp, vp, i32, i32, vp]
         L.aio_decode_greedy.argtypes = [vp, i32, i32, i32, vp, vp]
         L.aio_profile_step.argtypes = [vp, i32, i32, vp, vp, i32, P(i32)]
+        L.aio_trace_step.argtypes = [vp, i32, i32, vp, vp, i32, P(i32)]
+        L.aio_device_status.argtypes = [vp, P(i32)]
+        L.aio_uses_step_kernel.argtypes = [vp]
         _lib = L
     return _lib
 
@@ -185,6 +188,26 @@ def aio_profile_step(handle: int, token: int, pos: int, logits: torch.Tensor,
     return ms[: n.value].copy()
 
 
+def aio_trace_step(handle: int, token: int, pos: int, logits: torch.Tensor,
+                   max_phases: int) -> np.ndarray:
+    """Per-phase microseconds of one step of the persistent kernel."""
+    us = np.zeros(max_phases, dtype=np.float64)
+    n = ctypes.c_int32(0)
+    _check(lib().aio_trace_step(handle, int(token), int(pos), _ptr(logits), us.ctypes.data,
+                                int(max_phases), ctypes.byref(n)), "aio_trace_step")
+    return us[: n.value].copy()
+
+
+def aio_device_status(handle: int) -> int:
+    st = ctypes.c_int32(0)
+    _check(lib().aio_device_status(handle, ctypes.byref(st)), "aio_device_status")
+    return int(st.value)
+
+
+def aio_uses_step_kernel(handle: int) -> bool:
+    return bool(lib().aio_uses_step_kernel(handle))
+
+
 # ------------------------------------------------------------------ a model
 
 def _to_device(a: np.ndarray, device) -> torch.Tensor:
@@ -264,6 +287,17 @@ class DeviceModel:
 
     def profile_step(self, token: int, pos: int, logits: torch.Tensor) -> np.ndarray:
         return aio_profile_step(self.handle, token, pos, logits, 6 * self.c.n_layers + 1)
+
+    def trace_step(self, token: int, pos: int, logits: torch.Tensor) -> np.ndarray:
+        return aio_trace_step(self.handle, token, pos, logits, 5 * self.c.n_layers + 1)
+
+    @property
+    def uses_step_kernel(self) -> bool:
+        return aio_uses_step_kernel(self.handle)
+
+    def status(self) -> int:
+        """Device-side status word (0 = fine); synchronises."""
+        return aio_device_status(self.handle)
 
     def sync(self) -> None:
         self.stream.synchronize()

@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "aio.h"
+#include "step_kernel.h"
 
 // Device-resident decode state: the token(s) and position the next kernels
 // consume.  aio_decode_step writes it with a one-thread kernel; in greedy mode
@@ -30,8 +31,11 @@ struct WsLayout {
   size_t part_ml;  // fp32 [MV][H][S][2]      split-KV (max, sum) in log2 units
   size_t act;      // bf16 [2][32][KA]        split activations for the verify GEMM
   size_t amax;     // int32 [MV]              argmax scratch
+  size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters
+  size_t mega_part;  // fp32 [H][S_mega][hd+2] step-kernel split partials
   size_t total;
   int splits;      // S, split-KV partitions per head
+  int mega_splits; // S_mega, split-KV partitions per kv head in the step kernel
   int ka;          // KA = max(d, H*hd, F)
 };
 
@@ -54,6 +58,11 @@ struct aio_model {
   float* greedy_logits;        // logits pointer baked into greedy_exec
   int32_t* greedy_tokens;      // token output pointer baked into greedy_exec
   bool use_graph;
+  // persistent step kernel (one cooperative launch per decode step)
+  bool use_mega;
+  int mega_blocks;
+  MegaLayer* mega_layers;          // library-owned device table [n_layers]
+  unsigned long long* mega_trace;  // library-owned, allocated on first trace
   // profiling: when prof_ev is set, every launcher records one event after
   // each kernel it enqueues (aio_profile_step)
   mutable hipEvent_t* prof_ev;

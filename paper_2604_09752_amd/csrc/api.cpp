@@ -6,6 +6,7 @@
 
 #include <new>
 #include <string>
+#include <vector>
 
 #include "aio_internal.h"
 
@@ -63,6 +64,11 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * 2 * 4);
   L.act = off; off = align256(off + 2 * 32 * ka * 2);  // two split-activation buffers
   L.amax = off; off = align256(off + MV * 4);
+  L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
+  L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
+  if (L.mega_splits < 1) L.mega_splits = 1;
+  L.mega_part = off;
+  off = align256(off + (size_t)c.n_heads * (size_t)L.mega_splits * ((size_t)c.head_dim + 2) * 4);
   L.total = off;
   return L;
 }
@@ -188,6 +194,11 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
   m->greedy_tokens = nullptr;
   const char* g = getenv("AIO_GRAPH");
   m->use_graph = !(g && strcmp(g, "0") == 0) && hip_stream != nullptr;
+  const char* mg = getenv("AIO_MEGA");
+  m->use_mega = !(mg && strcmp(mg, "0") == 0) && aio_step_kernel_supports(*cfg) &&
+                prop.cooperativeLaunch;
+  m->mega_blocks = prop.multiProcessorCount < AIO_STEP_MAX_BLOCKS ? prop.multiProcessorCount
+                                                                   : AIO_STEP_MAX_BLOCKS;
 
   // RoPE table: cos/sin of pos * base^(-2i/hd), angles in double, stored fp32.
   const int half = cfg->head_dim / 2;
@@ -204,8 +215,31 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
   e = hipMalloc((void**)&m->rope, n * sizeof(float2));
   if (e == hipSuccess) e = hipMemcpy(m->rope, host, n * sizeof(float2), hipMemcpyHostToDevice);
   free(host);
+  if (e == hipSuccess && m->use_mega) {
+    std::vector<MegaLayer> tab((size_t)cfg->n_layers);
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      const aio_layer_weights& L = w->layers[l];
+      MegaLayer& t = tab[(size_t)l];
+      const void* mats[7] = {L.wq, L.wk, L.wv, L.wo, L.w_gate, L.w_up, L.w_down};
+      const void* scs[7] = {L.sq, L.sk, L.sv, L.so, L.s_gate, L.s_up, L.s_down};
+      for (int i = 0; i < 7; ++i) {
+        t.w[i] = mats[i];
+        t.s[i] = (const uint16_t*)scs[i];
+      }
+      t.attn_norm = (const uint16_t*)L.attn_norm;
+      t.ffn_norm = (const uint16_t*)L.ffn_norm;
+      t.kc = m->kv_layer(l, 0);
+      t.vc = m->kv_layer(l, 1);
+    }
+    e = hipMalloc((void**)&m->mega_layers, tab.size() * sizeof(MegaLayer));
+    if (e == hipSuccess)
+      e = hipMemcpy(m->mega_layers, tab.data(), tab.size() * sizeof(MegaLayer),
+                    hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
+  }
   if (e != hipSuccess) {
     if (m->rope) (void)hipFree(m->rope);
+    if (m->mega_layers) (void)hipFree(m->mega_layers);
     delete m;
     return hip_fail(e);
   }
@@ -221,10 +255,13 @@ void aio_model_free(aio_model* m) {
   }
   if (m->greedy_exec) (void)hipGraphExecDestroy(m->greedy_exec);
   if (m->rope) (void)hipFree(m->rope);
+  if (m->mega_layers) (void)hipFree(m->mega_layers);
+  if (m->mega_trace) (void)hipFree(m->mega_trace);
   delete m;
 }
 
 static hipError_t enqueue_step_body(aio_model* m, float* logits) {
+  if (m->use_mega) return aio_launch_step_kernel(*m, logits, nullptr, nullptr);
   hipError_t e;
   for (int l = 0; l < m->cfg.n_layers; ++l)
     if ((e = aio_launch_decode_layer(*m, l)) != hipSuccess) return e;
@@ -262,6 +299,7 @@ int aio_argmax(aio_model* m, const float* logits_dev, int32_t rows, int32_t n, i
 }
 
 static hipError_t enqueue_greedy_body(aio_model* m, float* logits, int32_t* tokens) {
+  if (m->use_mega) return aio_launch_step_kernel(*m, logits, tokens, nullptr);
   hipError_t e = enqueue_step_body(m, logits);
   if (e != hipSuccess) return e;
   return aio_launch_argmax(*m, logits, 1, m->cfg.vocab, tokens, true);
@@ -300,7 +338,7 @@ int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
   if (n_steps < 1 || (int64_t)pos + n_steps > (int64_t)m->cfg.max_ctx) return AIO_ERANGE;
   hipError_t e = aio_launch_set_state(*m, token, pos);
   if (e != hipSuccess) return hip_fail(e);
-  if (m->use_graph) {
+  if (m->use_graph && !m->use_mega) {
     if ((e = ensure_greedy_graph(m, logits_dev, tokens_dev)) != hipSuccess) return hip_fail(e);
     for (int s = 0; s < n_steps; ++s)
       if ((e = hipGraphLaunch(m->greedy_exec, m->stream)) != hipSuccess) return hip_fail(e);
@@ -317,7 +355,7 @@ int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev
     return AIO_EINVAL;
   int rc = aio_check_decode(&m->cfg, token, pos);
   if (rc) return rc;
-  const int need = 6 * m->cfg.n_layers + 1;
+  const int need = m->use_mega ? 1 : 6 * m->cfg.n_layers + 1;
   if (!m->prof_ev) {
     m->prof_ev = (hipEvent_t*)calloc((size_t)need + 1, sizeof(hipEvent_t));
     if (!m->prof_ev) return AIO_ENOMEM;
@@ -348,5 +386,53 @@ int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev
   *n_kernels = out;
   return AIO_OK;
 }
+
+int aio_trace_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, double* phase_us,
+                   int32_t max_phases, int32_t* n_phases) {
+  if (!m || !logits_dev || !aligned16(logits_dev) || !phase_us || !n_phases || max_phases < 1)
+    return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  if (!m->use_mega) return AIO_EUNSUPPORTED;
+  const int nb = 5 * m->cfg.n_layers + 1;  // barrier slots 1..5L, slot 0 unused
+  hipError_t e = hipSuccess;
+  if (!m->mega_trace) e = hipMalloc((void**)&m->mega_trace, (size_t)(nb + 1) * 8);
+  if (e == hipSuccess) e = hipMemsetAsync(m->mega_trace, 0, (size_t)(nb + 1) * 8, m->stream);
+  if (e == hipSuccess) e = aio_launch_set_state(*m, token, pos);
+  if (e == hipSuccess) e = aio_launch_step_kernel(*m, logits_dev, nullptr, m->mega_trace);
+  if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  std::vector<unsigned long long> t((size_t)nb + 1);
+  e = hipMemcpy(t.data(), m->mega_trace, t.size() * 8, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  int clk_khz = 0;
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (hipDeviceGetAttribute(&clk_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+      clk_khz <= 0)
+    clk_khz = 100000;
+  // barrier exits 1..5L bound 5L - 1 phases (the first QKV and the LM head
+  // lie outside them)
+  const int out = (nb - 2) < max_phases ? (nb - 2) : max_phases;
+  for (int i = 0; i < out; ++i)
+    phase_us[i] = (double)(t[(size_t)i + 2] - t[(size_t)i + 1]) * 1e3 / (double)clk_khz;
+  *n_phases = out;
+  return AIO_OK;
+}
+
+int aio_device_status(aio_model* m, int32_t* status) {
+  if (!m || !status) return AIO_EINVAL;
+  *status = 0;
+  if (!m->use_mega) return AIO_OK;
+  hipError_t e = hipStreamSynchronize(m->stream);
+  unsigned err = 0;
+  if (e == hipSuccess)
+    e = hipMemcpy(&err, m->ws + m->lay.sync + (size_t)kSyncErr * 4, 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  *status = (int32_t)err;
+  return AIO_OK;
+}
+
+int aio_uses_step_kernel(const aio_model* m) { return m && m->use_mega ? 1 : 0; }
 
 }  // extern "C"

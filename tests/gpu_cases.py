@@ -2,6 +2,7 @@
 the HIP path and the oracle, run teacher-forced steps on both, compare."""
 from __future__ import annotations
 
+import os
 import sys
 import time
 
@@ -19,17 +20,38 @@ def log(*a):
     sys.stdout.flush()
 
 
-class Pair:
-    """The HIP model and the oracle on identical seeded inputs."""
+class env_set:
+    """Temporarily set environment variables (read by the library at load)."""
 
-    def __init__(self, cfg, with_oracle: bool = True):
+    def __init__(self, **kw):
+        self.kw = {k: v for k, v in kw.items() if v is not None}
+
+    def __enter__(self):
+        self.old = {k: os.environ.get(k) for k in self.kw}
+        os.environ.update(self.kw)
+
+    def __exit__(self, *exc):
+        for k, v in self.old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+class Pair:
+    """The HIP model and the oracle on identical seeded inputs.  mega="1" /
+    "0" selects the persistent step kernel / the per-operation kernels."""
+
+    def __init__(self, cfg, with_oracle: bool = True, mega: str | None = None):
         from paper_2604_09752_amd.binding import DeviceModel
         t0 = time.time()
         self.cfg = cfg
         self.w = synth.make_weights(cfg)
         self.kv_host = synth.make_kv(cfg)
         log("[%s] inputs generated in %.1fs" % (cfg.name, time.time() - t0))
-        self.gpu = DeviceModel(cfg, self.w, kv_init=self.kv_host)
+        with env_set(AIO_MEGA=mega):
+            self.gpu = DeviceModel(cfg, self.w, kv_init=self.kv_host)
+        log("[%s] persistent step kernel: %s" % (cfg.name, self.gpu.uses_step_kernel))
         self.orc = oracle.OracleModel(cfg, self.w) if with_oracle else None
         self.logits = self.gpu.new_logits(cfg.max_verify)
         self.tok_out = torch.zeros(max(cfg.max_verify, 1), dtype=torch.int32,
@@ -49,7 +71,11 @@ class Pair:
     def oracle_step(self, token: int, pos: int) -> np.ndarray:
         return self.orc.decode_step(self.kv_host, token, pos)
 
+    def check_status(self):
+        assert self.gpu.status() == 0, "a grid barrier of the step kernel timed out"
+
     def close(self):
+        self.check_status()
         self.gpu.close()
         del self.gpu
         torch.cuda.empty_cache()

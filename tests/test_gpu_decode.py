@@ -19,9 +19,9 @@ pytestmark = pytest.mark.gpu
 TINY = synth.CONFIGS["tiny"]
 
 
-@pytest.fixture(scope="module")
-def tiny():
-    p = Pair(TINY)
+@pytest.fixture(scope="module", params=["1", "0"], ids=["step_kernel", "per_op"])
+def tiny(request):
+    p = Pair(TINY, mega=request.param)
     yield p
     p.close()
 
@@ -83,11 +83,12 @@ def int8_tol(ref_rms: float) -> float:
     return LOGIT_TOL * max(1.0, ref_rms)
 
 
+@pytest.mark.parametrize("mega", ["1", "0"], ids=["step_kernel", "per_op"])
 @pytest.mark.parametrize("name", list(VARIANTS))
-def test_shape_variants(name):
+def test_shape_variants(name, mega):
     kw = dict(VARIANTS[name])
     cfg = TINY.with_(name=name, prompt_len=40, n_steps=24, **kw)
-    pair = Pair(cfg)
+    pair = Pair(cfg, mega=mega)
     try:
         prompt = synth.make_prompt(cfg)
         tok, worst, agree = int(prompt[0]), 0.0, 0
@@ -142,21 +143,17 @@ def test_decode_is_deterministic(tiny):
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
-@pytest.mark.parametrize("use_graph", ["1", "0"])
-def test_greedy_loop_matches_step_by_step(use_graph):
+@pytest.mark.parametrize("use_graph,mega", [("1", "0"), ("0", "0"), ("0", "1")],
+                         ids=["per_op_graph", "per_op_direct", "step_kernel"])
+def test_greedy_loop_matches_step_by_step(use_graph, mega):
     from paper_2604_09752_amd.binding import DeviceModel
+    from tests.gpu_cases import env_set
     cfg = TINY.with_(name="greedy", prompt_len=16, n_steps=24)
     w = synth.make_weights(cfg)
-    old = os.environ.get("AIO_GRAPH")
-    os.environ["AIO_GRAPH"] = use_graph
-    try:
+    with env_set(AIO_GRAPH=use_graph, AIO_MEGA=mega):
         g1 = DeviceModel(cfg, w)
         g2 = DeviceModel(cfg, w)
-    finally:
-        if old is None:
-            os.environ.pop("AIO_GRAPH")
-        else:
-            os.environ["AIO_GRAPH"] = old
+    assert g1.uses_step_kernel == (mega == "1")
     prompt = synth.make_prompt(cfg)
     lg1, lg2 = g1.new_logits(), g2.new_logits()
     for p, t in enumerate(prompt):
@@ -187,6 +184,7 @@ def test_greedy_loop_matches_step_by_step(use_graph):
         g2.sync()
         tok = int(one.item())
         assert int(toks2[s].item()) == tok
+    assert g1.status() == 0 and g2.status() == 0
     g1.close()
     g2.close()
 
