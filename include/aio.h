@@ -207,6 +207,16 @@ int aio_uses_step_kernel(const aio_model* m);
 int aio_trace_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, double* phase_us,
                    int32_t max_phases, int32_t* n_phases);
 
+/* Barrier timing of one step of the persistent kernel: every workgroup
+ * records the device clock (100 MHz) when it arrives at and leaves each grid
+ * barrier.  arrive and leave (host arrays of max_entries >= (5 L + 1) x
+ * blocks) receive [barrier][workgroup] times (barrier 0 unused); n_barriers
+ * and n_blocks the dimensions.  Allocates a device buffer and synchronises;
+ * a profiling aid.  AIO_EUNSUPPORTED when the handle does not use that kernel. */
+int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
+                       uint64_t* arrive, uint64_t* leave, int32_t max_entries,
+                       int32_t* n_barriers, int32_t* n_blocks);
+
 /* Synchronises the model's stream and reports the device-side status word:
  * 0, or 1 if a grid barrier of the persistent kernel gave up waiting (its
  * results are then invalid).  Synchronises. */

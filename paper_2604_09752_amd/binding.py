@@ -79,6 +79,7 @@ def lib():
         L.aio_profile_step.argtypes = [vp, i32, i32, vp, vp, i32, P(i32)]
         L.aio_trace_step.argtypes = [vp, i32, i32, vp, vp, i32, P(i32)]
         L.aio_device_status.argtypes = [vp, P(i32)]
+        L.aio_trace_barriers.argtypes = [vp, i32, i32, vp, vp, vp, i32, P(i32), P(i32)]
         L.aio_uses_step_kernel.argtypes = [vp]
         _lib = L
     return _lib
@@ -196,6 +197,20 @@ def aio_trace_step(handle: int, token: int, pos: int, logits: torch.Tensor,
     _check(lib().aio_trace_step(handle, int(token), int(pos), _ptr(logits), us.ctypes.data,
                                 int(max_phases), ctypes.byref(n)), "aio_trace_step")
     return us[: n.value].copy()
+
+
+def aio_trace_barriers(handle: int, token: int, pos: int, logits: torch.Tensor, n_layers: int,
+                       max_blocks: int = 1024):
+    """(arrive, leave) device-clock times [barrier][workgroup] of one step."""
+    cap = (5 * n_layers + 1) * max_blocks
+    arr = np.zeros(cap, dtype=np.uint64)
+    lev = np.zeros(cap, dtype=np.uint64)
+    nb, nk = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().aio_trace_barriers(handle, int(token), int(pos), _ptr(logits), arr.ctypes.data,
+                                    lev.ctypes.data, cap, ctypes.byref(nb), ctypes.byref(nk)),
+           "aio_trace_barriers")
+    n = nb.value * nk.value
+    return arr[:n].reshape(nb.value, nk.value), lev[:n].reshape(nb.value, nk.value)
 
 
 def aio_device_status(handle: int) -> int:

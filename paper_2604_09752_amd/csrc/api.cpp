@@ -420,6 +420,35 @@ int aio_trace_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, 
   return AIO_OK;
 }
 
+int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
+                       uint64_t* arrive, uint64_t* leave, int32_t max_entries,
+                       int32_t* n_barriers, int32_t* n_blocks) {
+  if (!m || !logits_dev || !aligned16(logits_dev) || !arrive || !leave || !n_barriers ||
+      !n_blocks)
+    return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  if (!m->use_mega) return AIO_EUNSUPPORTED;
+  const int nbar = 5 * m->cfg.n_layers + 1, nblk = m->mega_blocks;
+  const size_t n = (size_t)nbar * (size_t)nblk;
+  if ((size_t)max_entries < n) return AIO_ERANGE;
+  unsigned long long* dev = nullptr;  // arrive [n], leave [n], detail [n][2]
+  hipError_t e = hipMalloc((void**)&dev, 4 * n * 8);
+  if (e == hipSuccess) e = hipMemsetAsync(dev, 0, 4 * n * 8, m->stream);
+  if (e == hipSuccess) e = aio_launch_set_state(*m, token, pos);
+  if (e == hipSuccess) e = aio_launch_step_kernel(*m, logits_dev, nullptr, nullptr, dev, dev + n);
+  if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+  if (e == hipSuccess) e = hipMemcpy(arrive, dev, n * 8, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(leave, dev + n, n * 8, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && (size_t)max_entries >= 4 * n)  // room for the detail times too
+    e = hipMemcpy(arrive + n, dev + 2 * n, 2 * n * 8, hipMemcpyDeviceToHost);
+  if (dev) (void)hipFree(dev);
+  if (e != hipSuccess) return hip_fail(e);
+  *n_barriers = nbar;
+  *n_blocks = nblk;
+  return AIO_OK;
+}
+
 int aio_device_status(aio_model* m, int32_t* status) {
   if (!m || !status) return AIO_EINVAL;
   *status = 0;

@@ -52,6 +52,9 @@ struct MegaArgs {
   float* logits;   // [V]
   int32_t* tokens_out;
   unsigned long long* trace;  // optional: barrier exit times (workgroup 0), [5 L + 1]
+  unsigned long long* bar_arrive;  // optional: [5 L + 1][blocks] arrival times
+  unsigned long long* bar_leave;   // optional: [5 L + 1][blocks] exit times
+  unsigned long long* detail;      // optional: [5 L + 1][blocks][2] input-ready, loop-done
   int L, d, H, Hkv, hd, F, V, max_ctx, S;
   float eps, scale_log2;
 };
@@ -60,4 +63,6 @@ bool aio_step_kernel_supports(const aio_config& c);
 int aio_step_kernel_vpl(const aio_config& c, int K);
 size_t aio_step_kernel_lds(const aio_config& c, int blocks);
 hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* tokens_out,
-                                  unsigned long long* trace);
+                                  unsigned long long* trace,
+                                  unsigned long long* bar_arrive = nullptr,
+                                  unsigned long long* bar_leave = nullptr);

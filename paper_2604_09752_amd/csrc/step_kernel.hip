@@ -23,7 +23,9 @@
 // Matrix phases: the rows of a matrix are split evenly over workgroups; the
 // 8 waves of a workgroup split K, so each lane keeps only its slice of the
 // activation in registers; per-wave partial sums meet in LDS.  Weights are
-// double-buffered in registers, 8 loads of 16 bytes per lane per batch.
+// double-buffered in registers, 8 loads of 16 bytes per lane per batch, and
+// every wait for a buffer names only the loads issued before it (the loops
+// are branch-free and nothing else is loaded inside them).
 //
 // Coherence: the 8 XCDs have separate L2 caches that are not kept coherent
 // with each other, and a device-scope fence (L2 write-back + invalidate)
@@ -49,7 +51,15 @@ namespace {
 constexpr int kT = 512;          // threads per workgroup
 constexpr int kW = kT / AIO_WAVE; // waves per workgroup
 constexpr int kNLD = 8;          // 16-byte weight loads per lane per batch
+// Batches in flight per wave (register buffers).  Three stream the loops
+// faster but lose overall: the barrier's polling loads are queued behind the
+// prefetched weight loads (vector memory returns in order), so a deeper
+// prefetch delays every workgroup's view of the release.
+constexpr int kNBUF = 2;
 constexpr unsigned kSpinLimit = 1u << 17;  // ~0.1-0.2 s of polling
+// s_waitcnt immediate for vmcnt(0) with expcnt and lgkmcnt left at their
+// maximum (no wait): vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8].
+constexpr int kVmcnt0 = 0x0F70;
 
 enum Kind { K_QKV = 0, K_O = 1, K_GU = 2, K_DOWN = 3, K_LM = 4 };
 
@@ -95,11 +105,18 @@ AIO_DEV void spin_ge(const MegaArgs& a, const unsigned* p, unsigned target) {
 
 // Grid barrier: every workgroup raises its flag to `epoch`; workgroup 0
 // gathers all flags and raises the release word; everyone waits for it.
-AIO_DEV void grid_sync(const MegaArgs& a, unsigned ep0, unsigned k) {
+// The release fence before the flag is an s_waitcnt on every outstanding
+// vector memory operation (loads included), so `prefetch` -- the first
+// weight loads of the next phase -- is issued only after the flag is up; it
+// then proceeds while the workgroup waits for the release.
+template <class F>
+AIO_DEV void grid_sync(const MegaArgs& a, unsigned ep0, unsigned k, F&& prefetch) {
   const unsigned epoch = ep0 + k;
   wg_publish();
   const int tid = threadIdx.x;
+  if (a.bar_arrive && tid == 0) a.bar_arrive[(size_t)k * gridDim.x + blockIdx.x] = wall_clock64();
   if (tid == 0) st_dev(a.sync + kSyncFlags + blockIdx.x, epoch);
+  prefetch();
   if (blockIdx.x == 0) {
     for (int i = tid; i < (int)gridDim.x; i += kT) spin_ge(a, a.sync + kSyncFlags + i, epoch);
     __syncthreads();
@@ -108,9 +125,21 @@ AIO_DEV void grid_sync(const MegaArgs& a, unsigned ep0, unsigned k) {
   if (tid == 0) spin_ge(a, a.sync + kSyncRelease, epoch);
   __syncthreads();
   if (a.trace && blockIdx.x == 0 && tid == 0) a.trace[k] = wall_clock64();
+  if (a.bar_leave && tid == 0) a.bar_leave[(size_t)k * gridDim.x + blockIdx.x] = wall_clock64();
 }
 
 // ------------------------------------------------------------- matrix phase
+
+// The per-layer pointer table is read-only during the step; reading it
+// through the constant address space gives scalar loads, which complete on
+// their own counter.  A vector load here would be queued behind the weight
+// loads already in flight, and the first use of the pointer inside a weight
+// loop would then wait for all of them.
+typedef __attribute__((address_space(4))) const MegaLayer CMegaLayer;
+AIO_DEV const CMegaLayer* layer_at(const MegaArgs& a, int layer) {
+  return (const CMegaLayer*)(a.layers + layer);
+}
+
 
 typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
 
@@ -130,7 +159,7 @@ struct GPhase {
   int K;                   // input length
   int nvw;                 // 16-byte vectors in one wave's K-slice
   int u0, u1;              // this workgroup's units
-  int nb;                  // batches
+  int nu;                  // units of the whole phase
 };
 
 template <int WFMT>
@@ -149,7 +178,7 @@ AIO_DEV int n_units(const MegaArgs& a) {
 template <int WFMT, int KIND>
 AIO_DEV GPhase make_phase(const MegaArgs& a, int layer) {
   GPhase P;
-  const MegaLayer* L = a.layers + (layer < a.L ? layer : 0);
+  const CMegaLayer* L = layer_at(a, layer < a.L ? layer : 0);
   P.w1 = P.w2 = nullptr;
   P.s1 = P.s2 = nullptr;
   if (KIND == K_QKV) {
@@ -170,10 +199,21 @@ AIO_DEV GPhase make_phase(const MegaArgs& a, int layer) {
   }
   P.nvw = P.K / (kW * epv<WFMT>());
   const int nu = n_units<KIND>(a);
+  P.nu = nu;
   const int b = blockIdx.x, nbk = gridDim.x;
   P.u0 = (int)((long long)b * nu / nbk);
   P.u1 = (int)((long long)(b + 1) * nu / nbk);
   return P;
+}
+
+// One of three pointers, blended arithmetically: written as a select among
+// fields of a struct the compiler builds a lookup table in scratch memory,
+// and the scratch load then waits behind every weight load in flight.
+template <class T>
+AIO_DEV T* pick3(int i, T* p0, T* p1, T* p2) {
+  const uint64_t b0 = (uint64_t)p0;
+  const uint64_t d1 = (uint64_t)p1 - b0, d2 = (uint64_t)p2 - b0;
+  return (T*)(b0 + (uint64_t)(i == 1) * d1 + (uint64_t)(i == 2) * d2);
 }
 
 // Row r of unit u as (matrix base, row index in it, scale array).
@@ -192,13 +232,7 @@ AIO_DEV const char* row_base(const MegaArgs& a, const GPhase& P, int u, int r) {
   } else if (KIND == K_GU) {
     mat = r;
   }
-  // Blend the base arithmetically: written as a select among three pointers
-  // the compiler builds a lookup table in scratch memory, and the scratch
-  // load then waits behind every weight load in flight.
-  const uint64_t b0 = (uint64_t)P.w0;
-  const uint64_t d1 = (uint64_t)P.w1 - b0, d2 = (uint64_t)P.w2 - b0;
-  const uint64_t base = b0 + (uint64_t)(mat == 1) * d1 + (uint64_t)(mat == 2) * d2;
-  return (const char*)base + (size_t)row * (size_t)P.K * wb;
+  return pick3(mat, P.w0, P.w1, P.w2) + (size_t)row * (size_t)P.K * wb;
 }
 
 // The row base is the same for every lane of a wave; say so, so that the
@@ -210,23 +244,43 @@ AIO_DEV const char* wave_uniform(const char* p) {
   return (const char*)(((uint64_t)hi << 32) | lo);
 }
 
+// This thread's position.  Each phase takes a fresh copy that the compiler
+// cannot see through, so values derived from it (per-lane offsets, shuffle
+// addresses) are recomputed in the phase that uses them instead of being
+// hoisted out of the layer loop and kept live -- and spilled -- across the
+// whole kernel.
+struct Thr {
+  int tid, lane, wave;
+};
+AIO_DEV Thr thr() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return Thr{t, t & (AIO_WAVE - 1), t / AIO_WAVE};
+}
+
+// Whether load slot (unit u, vector vi) of a batch carries data.
+AIO_DEV bool slot_ok(const GPhase& P, int u, int vi) { return u < P.u1 && vi < P.nvw; }
+
+// Issue one batch.  Every slot is loaded unconditionally (an empty slot reads
+// the first vector of a row the workgroup streams anyway, a cache hit) and
+// masked when consumed: loads under branches would leave the compiler unable
+// to count the loads in flight, and it would then wait for all of them --
+// both buffers -- before every batch.
 template <int WFMT, int KIND, int VPL, int HD>
-AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[kNLD]) {
+AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[kNLD], const Thr& T) {
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
-  const int lane = threadIdx.x & (AIO_WAVE - 1), wave = threadIdx.x / AIO_WAVE;
+  const int lane = T.lane, wave = T.wave;
+  const int ulast = P.nu - 1;
 #pragma unroll
-  for (int j = 0; j < kNLD; ++j) {
+  for (int j = 0; j < UB * RPU * VPL; ++j) {
     const int ul = j / (RPU * VPL), r = (j / VPL) % RPU, v = j % VPL;
     const int u = P.u0 + batch * UB + ul;
     const int vi = v * AIO_WAVE + lane;
-    if (j < UB * RPU * VPL && u < P.u1 && vi < P.nvw) {
-      const char* rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u, r));
-      const uint4* p = (const uint4*)rb + (size_t)wave * P.nvw + vi;
-      buf[j] = ldg_stream(p);
-    } else {
-      buf[j] = make_uint4(0u, 0u, 0u, 0u);
-    }
+    const bool ok = slot_ok(P, u, vi);
+    const char* rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, r));
+    const uint4* p = (const uint4*)rb + (size_t)wave * P.nvw + (ok ? vi : 0);
+    buf[j] = ldg_stream(p);
   }
 }
 
@@ -234,9 +288,8 @@ AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[k
 // exchange (offsets 32, 16, 8) keeps half of the values, so lane l ends with
 // value (l >> 3) & 7 summed over 8 lanes; three plain exchanges finish the
 // sum (10 shuffles for 8 values instead of 48).
-AIO_DEV float reduce_rows(float (&v)[kNLD]) {
+AIO_DEV float reduce_rows(float (&v)[kNLD], int lane) {
   static_assert(kNLD == 8, "reduce_rows assumes 8 values");
-  const int lane = threadIdx.x & (AIO_WAVE - 1);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const bool up = lane & 32;
@@ -262,13 +315,16 @@ AIO_DEV float reduce_rows(float (&v)[kNLD]) {
 }
 
 // Multiply-accumulate one batch and leave each wave's row partials in LDS
-// red[(local unit * RPU + r) * kW + wave].
+// red[(local unit * RPU + r) * kW + wave].  Slots are not masked here: a
+// lane past the end of its K-slice holds h = 0 (load_input) and reads a
+// vector of the same row, so it adds an exact zero for finite weights; a
+// unit past the workgroup's range is dropped at the LDS write.
 template <int WFMT, int KIND, int VPL>
 AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
-                     const float (&h)[VPL][epv<WFMT>()], float* red) {
+                     const float (&h)[VPL][epv<WFMT>()], float* red, const Thr& T) {
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
-  const int lane = threadIdx.x & (AIO_WAVE - 1), wave = threadIdx.x / AIO_WAVE;
+  const int lane = T.lane, wave = T.wave;
   float acc[kNLD];
 #pragma unroll
   for (int i = 0; i < kNLD; ++i) acc[i] = 0.f;
@@ -287,7 +343,7 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
       t = dot4_i8(w.w, make_float4(h[v][12], h[v][13], h[v][14], h[v][15]), t);
     }
   }
-  const float s = reduce_rows(acc);
+  const float s = reduce_rows(acc, lane);
   const int idx = (lane >> 3) & 7;
   if ((lane & 7) == 0 && idx < UB * RPU) {
     const int ul = idx / RPU, r = idx % RPU;
@@ -301,9 +357,9 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
 // [(w * nvw + v * 64 + lane) * EPV, +EPV).
 template <int WFMT, int KIND, int VPL>
 AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token,
-                        float (&h)[VPL][epv<WFMT>()], float* red8) {
+                        float (&h)[VPL][epv<WFMT>()], float* red8, const Thr& T) {
   constexpr int E = epv<WFMT>();
-  const int lane = threadIdx.x & (AIO_WAVE - 1), wave = threadIdx.x / AIO_WAVE;
+  const int lane = T.lane, wave = T.wave;
   const float* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : a.x);
   const bool emb = KIND == K_QKV && layer == 0;
   float ss = 0.f;
@@ -339,7 +395,7 @@ AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token
     for (int w = 0; w < kW; ++w) tot += red8[w];
     __syncthreads();  // red8 is reused by the next phase
     const float inv = rsqrtf(tot / (float)P.K + a.eps);
-    const MegaLayer* L = a.layers + (layer < a.L ? layer : 0);
+    const CMegaLayer* L = layer_at(a, layer < a.L ? layer : 0);
     const uint16_t* g = KIND == K_QKV ? L->attn_norm : (KIND == K_GU ? L->ffn_norm : a.final_norm);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
@@ -389,10 +445,10 @@ struct Smem {
 // phase-specific output.
 template <int WFMT, int KIND>
 AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, const float* red,
-                      Smem& sm) {
+                      Smem& sm, float xpre, const Thr& T) {
   constexpr int RPU = rpu_of<KIND>();
   const int nu = P.u1 - P.u0;
-  const int tid = threadIdx.x;
+  const int tid = T.tid;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
   for (int t = tid; t < nu; t += kT) {
@@ -414,7 +470,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
       else if (vlo >= qrows) { sec = 1; rlo -= qrows; }
       // y[0] = dim i, y[1] = dim i+1, y[2] = dim i+half, y[3] = dim i+1+half
       if constexpr (WFMT == AIO_WFMT_INT8) {
-        const uint16_t* sc = sec == 0 ? P.s0 : (sec == 1 ? P.s1 : P.s2);
+        const uint16_t* sc = pick3(sec, P.s0, P.s1, P.s2);
         y[0] *= fp16_to_f32(sc[rlo]);
         y[1] *= fp16_to_f32(sc[rlo + 1]);
         y[2] *= fp16_to_f32(sc[rlo + half]);
@@ -436,7 +492,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         stf_dev(a.q + rlo + half + 1, y[3]);
       } else {
         const int g = rlo / a.hd, ii = rlo % a.hd;
-        const MegaLayer* L = a.layers + layer;
+        const CMegaLayer* L = layer_at(a, layer);
         uint16_t* c = (sec == 1 ? L->kc : L->vc) + ((size_t)g * a.max_ctx + pos) * a.hd;
         st_dev((unsigned*)(c + ii), (unsigned)f32_to_bf16(y[0]) | ((unsigned)f32_to_bf16(y[1]) << 16));
         st_dev((unsigned*)(c + ii + half),
@@ -456,7 +512,8 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         a.logits[u] = yy;
         if (am_better(yy, u, bv, bi)) { bv = yy; bi = u; }
       } else {
-        stf_dev(a.x + u, ldf_dev(a.x + u) + yy);
+        const float xo = t == tid ? xpre : ldf_dev(a.x + u);
+        stf_dev(a.x + u, xo + yy);
       }
     }
   }
@@ -492,37 +549,56 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
   }
 }
 
-// One matrix phase.  On entry A holds (in flight) batch 0 of this phase;
-// on exit A holds batch 0 of `NEXT` (if any) of layer `next_layer`.
-template <int WFMT, int HD, int KIND, int VPL, int NEXT, int NVPL>
-AIO_DEV void gemv_phase(const MegaArgs& a, const GPhase& P, int layer, int next_layer, int pos,
-                        int token, uint4 (&A)[kNLD], uint4 (&B)[kNLD], float* red, Smem& sm) {
+// The register buffers of a wave: kNBUF batches of kNLD 16-byte loads.
+struct Bufs {
+  uint4 b[kNBUF][kNLD];
+};
+
+// One matrix phase.  On entry buffer j holds (in flight) batch j of this
+// phase; each buffer is refilled with the phase's batch kNBUF further on as
+// soon as it is consumed.
+template <int WFMT, int HD, int KIND, int VPL>
+AIO_DEV void gemv_phase(const MegaArgs& a, const GPhase& P, int layer, int pos, int token,
+                        Bufs& W, float* red, Smem& sm, unsigned kb) {
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
   const int nb = (P.u1 - P.u0 + UB - 1) / UB;
-  if (nb > 1) issue<WFMT, KIND, VPL, HD>(a, P, 1, B);
+  const Thr T = thr();
+  // residual rows this workgroup will update, fetched now to hide the trip
+  float xpre = 0.f;
+  if (KIND == K_O || KIND == K_DOWN) {
+    if (T.tid < P.u1 - P.u0) xpre = ldf_dev(a.x + P.u0 + T.tid);
+  }
   float h[VPL][epv<WFMT>()];
-  load_input<WFMT, KIND, VPL>(a, P, layer, token, h, sm.red8);
-  bool next_done = false;
-  auto prefetch_next = [&]() {
-    if constexpr (NEXT >= 0) {
-      const GPhase N = make_phase<WFMT, NEXT>(a, next_layer);
-      issue<WFMT, NEXT, NVPL, HD>(a, N, 0, A);
-    }
-    next_done = true;
-  };
-  for (int b = 0; b < nb; b += 2) {
-    compute<WFMT, KIND, VPL>(P, b, A, h, red);
-    if (b + 2 < nb) issue<WFMT, KIND, VPL, HD>(a, P, b + 2, A);
-    else prefetch_next();
-    if (b + 1 < nb) {
-      compute<WFMT, KIND, VPL>(P, b + 1, B, h, red);
-      if (b + 3 < nb) issue<WFMT, KIND, VPL, HD>(a, P, b + 3, B);
+  load_input<WFMT, KIND, VPL>(a, P, layer, token, h, sm.red8, T);
+  if (a.detail && T.tid == 0) a.detail[((size_t)kb * gridDim.x + blockIdx.x) * 2] = wall_clock64();
+  // The input loads above were issued after this phase's first batches,
+  // so waiting for them has waited for everything; say so explicitly
+  // (vmcnt(0)), so that the loop below starts from a state in which only
+  // its own loads are in flight and waits only for the buffer it consumes.
+  __builtin_amdgcn_s_waitcnt(kVmcnt0);
+  // Branch-free body: a batch past the end is computed fully masked and its
+  // refill is a masked dummy (cache-hit) load, so the compiler sees the same
+  // loads in flight behind each buffer on every path.
+  for (int b = 0; b < nb; b += kNBUF) {
+#pragma unroll
+    for (int j = 0; j < kNBUF; ++j) {
+      compute<WFMT, KIND, VPL>(P, b + j, W.b[j], h, red, T);
+      issue<WFMT, KIND, VPL, HD>(a, P, b + j + kNBUF, W.b[j], T);
     }
   }
-  if (!next_done) prefetch_next();
   __syncthreads();
-  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm);
+  if (a.detail && T.tid == 0) a.detail[((size_t)kb * gridDim.x + blockIdx.x) * 2 + 1] = wall_clock64();
+  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, T);
+}
+
+// Issue the first kNBUF batches of a matrix phase into the buffers.
+template <int WFMT, int HD, int KIND, int VPL>
+AIO_DEV void prefetch(const MegaArgs& a, int layer, Bufs& W) {
+  const GPhase N = make_phase<WFMT, KIND>(a, layer);
+  const Thr T = thr();
+#pragma unroll
+  for (int j = 0; j < kNBUF; ++j) issue<WFMT, KIND, VPL, HD>(a, N, j, W.b[j], T);
 }
 
 // ---------------------------------------------------------------- attention
@@ -534,10 +610,33 @@ AIO_DEV uint4 ldg16(const uint16_t* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// Online-softmax update of one group with one key row (already loaded).
+// One DPP lane move of a float (a VALU operation: no LDS round trip).
+template <int CTRL>
+AIO_DEV float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of 8 or 16 lanes; every lane of a group receives
+// the same total.  Each step adds a lane's value to that of a partner in the
+// other half of its current group: lane ^ 1, lane ^ 2 (quad permutations),
+// then the mirror lane of the other quad (row_half_mirror) and, for 16, of
+// the other half row (row_mirror).
+template <int WIDTH>
+AIO_DEV float group_sum_dpp(float v) {
+  static_assert(WIDTH == 8 || WIDTH == 16, "DPP sums cover 8 or 16 lanes");
+  v += dpp_mov<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  if (WIDTH == 16) v += dpp_mov<0x140>(v);  // row_mirror
+  return v;
+}
+
+// Online-softmax update of one group with one key row (already loaded).  A
+// key past the group's range (valid false) leaves the state unchanged; the
+// masking is done with selects so that the loop has no divergent branches.
 template <int HD, int G>
-AIO_DEV void attend_key(const uint4 kk, const uint4 vv, const float (&q)[G][8], float (&o)[G][8],
-                        float (&m)[G], float (&l)[G]) {
+AIO_DEV void attend_key(const uint4 kk, const uint4 vv, bool valid, const float (&q)[G][8],
+                        float (&o)[G][8], float (&m)[G], float (&l)[G]) {
   constexpr int LPK = HD / 8;
   const float vf[8] = {bf16_lo(vv.x), bf16_hi(vv.x), bf16_lo(vv.y), bf16_hi(vv.y),
                        bf16_lo(vv.z), bf16_hi(vv.z), bf16_lo(vv.w), bf16_hi(vv.w)};
@@ -545,9 +644,10 @@ AIO_DEV void attend_key(const uint4 kk, const uint4 vv, const float (&q)[G][8], 
   for (int gg = 0; gg < G; ++gg) {
     float sc = dot8_bf16(kk, make_float4(q[gg][0], q[gg][1], q[gg][2], q[gg][3]),
                          make_float4(q[gg][4], q[gg][5], q[gg][6], q[gg][7]), 0.f);
-    sc = group_sum<LPK>(sc);
-    const float mn = fmaxf(m[gg], sc);
-    const float c = exp2f(m[gg] - mn), p = exp2f(sc - mn);
+    sc = group_sum_dpp<LPK>(sc);
+    const float mn = valid ? fmaxf(m[gg], sc) : m[gg];
+    const float c = valid ? exp2f(m[gg] - mn) : 1.f;
+    const float p = valid ? exp2f(sc - mn) : 0.f;
     l[gg] = l[gg] * c + p;
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[gg][i] = fmaf(p, vf[i], o[gg][i] * c);
@@ -555,75 +655,88 @@ AIO_DEV void attend_key(const uint4 kk, const uint4 vv, const float (&q)[G][8], 
   }
 }
 
+// Four keys of a group: their K and V rows.
+struct KV4 {
+  uint4 k[4], v[4];
+};
+
 // Workgroup unit = (kv head g, split s) of the keys [0, pos].  HD/8 lanes
-// hold one key row; each group of lanes runs an online softmax over its keys
-// (4 keys per step, the next 4 loaded while these are processed), the groups
-// combine in LDS, and the split's (max, sum, unnormalised output) goes out
-// as a partial.  The last split of a kv head to finish merges the S partials
-// into o.
+// hold one key row; each group of lanes runs an online softmax over its keys,
+// the groups combine in LDS, and the split's (max, sum, unnormalised output)
+// goes out as a partial.  The last split of a kv head to finish merges the S
+// partials into o.  Keys stream through two sets of registers in turn (four
+// keys each): one set is in flight while the other is consumed, with no
+// copies between them, so the loads of the next keys are never waited for
+// early.  The first keys are requested before q, the group combine is split
+// four ways, and the merge loads all partials before reducing them.
 template <int HD, int G>
-AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos,
-                                                     float* lds, Smem& sm) {
+AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem& sm) {
   constexpr int LPK = HD / 8, NGR = kT / LPK;
-  float* sm_m = lds;                    // [NGR][G]
-  float* sm_l = lds + NGR * G;          // [NGR][G]
-  float* sm_o = lds + 2 * NGR * G;      // [NGR][G][HD]
-  const int tid = threadIdx.x, gi = tid / LPK, li = tid % LPK;
-  const MegaLayer* L = a.layers + layer;
+  constexpr int NOUT = G * HD;            // outputs of a unit
+  constexpr int R = kT / NOUT > 0 ? kT / NOUT : 1;  // threads per output
+  static_assert(NGR % R == 0, "groups must split evenly");
+  float* sm_m = lds;                      // [NGR][G]
+  float* sm_l = lds + NGR * G;            // [NGR][G]
+  float* sm_o = lds + 2 * NGR * G;        // [NGR][G][HD]
+  float* sm_r = sm_o + NGR * G * HD;      // [R][NOUT] partial sums, then merge scratch
+  const int tid = thr().tid, gi = tid / LPK, li = tid % LPK;
+  const CMegaLayer* L = layer_at(a, layer);
   const int S = a.S, units = a.Hkv * S;
   const int n_keys = pos + 1;
   const int chunk = (n_keys + S - 1) / S;
   for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
     const int g = unit / S, s = unit % S;
     const int j0 = s * chunk, j1 = min(n_keys, j0 + chunk);
+    // keys of this group: j = j0 + gi + t * NGR for t < nk.  Loads are
+    // unconditional: key t >= nk reads the last valid key of the split (a
+    // cache hit) and is masked when consumed.
+    const int nk = j1 - j0 > gi ? (j1 - j0 - gi + NGR - 1) / NGR : 0;
+    const int jlast = j1 > j0 ? j1 - 1 : (n_keys - 1);  // a key row of this kv head
+    const uint16_t* kb = L->kc + (size_t)g * a.max_ctx * HD + li * 8;
+    const uint16_t* vb = L->vc + (size_t)g * a.max_ctx * HD + li * 8;
+    auto load4 = [&](KV4& d, int t0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + i;
+        const size_t off = (size_t)(t < nk ? j0 + gi + t * NGR : jlast) * HD;
+        d.k[i] = ldg16(kb + off);
+        d.v[i] = ldg16(vb + off);
+      }
+    };
+    KV4 X, Y;
+    load4(X, 0);
     float q[G][8], o[G][8], m[G], l[G];
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) {
       const float* qp = a.q + (size_t)(g * G + gg) * HD + li * 8;
 #pragma unroll
+      for (int i = 0; i < 8; ++i) q[gg][i] = ldf_dev(qp + i);
+    }
+#pragma unroll
+    for (int gg = 0; gg < G; ++gg) {
+#pragma unroll
       for (int i = 0; i < 8; ++i) {
-        q[gg][i] = ldf_dev(qp + i) * a.scale_log2;
+        q[gg][i] *= a.scale_log2;
         o[gg][i] = 0.f;
       }
       m[gg] = -INFINITY;
       l[gg] = 0.f;
     }
-    // keys of this group: j = j0 + gi + t * NGR for t < nk
-    const size_t stride = (size_t)NGR * HD;
-    const uint16_t* kp = L->kc + ((size_t)g * a.max_ctx + j0 + gi) * HD + li * 8;
-    const uint16_t* vp = L->vc + ((size_t)g * a.max_ctx + j0 + gi) * HD + li * 8;
-    const int nk = j1 - j0 > gi ? (j1 - j0 - gi + NGR - 1) / NGR : 0;
-    int t = 0;
-    uint4 k0, k1, k2, k3, v0, v1, v2, v3;
-    if (t + 4 <= nk) {
-      k0 = ldg16(kp); v0 = ldg16(vp);
-      k1 = ldg16(kp + stride); v1 = ldg16(vp + stride);
-      k2 = ldg16(kp + 2 * stride); v2 = ldg16(vp + 2 * stride);
-      k3 = ldg16(kp + 3 * stride); v3 = ldg16(vp + 3 * stride);
+    // The scheduling barriers keep each set's loads where they are written:
+    // hoisted together, both sets would be waited for at the top of the loop.
+    for (int t = 0; t < nk; t += 8) {
+      load4(Y, t + 4);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) attend_key<HD, G>(X.k[i], X.v[i], t + i < nk, q, o, m, l);
+      __builtin_amdgcn_sched_barrier(0);
+      load4(X, t + 8);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < nk, q, o, m, l);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    while (t + 4 <= nk) {
-      // next four keys in flight while these four are processed
-      uint4 n0, n1, n2, n3, w0, w1, w2, w3;
-      const bool more = t + 8 <= nk;
-      if (more) {
-        const size_t o4 = (size_t)(t + 4) * stride;
-        n0 = ldg16(kp + o4); w0 = ldg16(vp + o4);
-        n1 = ldg16(kp + o4 + stride); w1 = ldg16(vp + o4 + stride);
-        n2 = ldg16(kp + o4 + 2 * stride); w2 = ldg16(vp + o4 + 2 * stride);
-        n3 = ldg16(kp + o4 + 3 * stride); w3 = ldg16(vp + o4 + 3 * stride);
-      }
-      attend_key<HD, G>(k0, v0, q, o, m, l);
-      attend_key<HD, G>(k1, v1, q, o, m, l);
-      attend_key<HD, G>(k2, v2, q, o, m, l);
-      attend_key<HD, G>(k3, v3, q, o, m, l);
-      t += 4;
-      if (!more) break;
-      k0 = n0; k1 = n1; k2 = n2; k3 = n3;
-      v0 = w0; v1 = w1; v2 = w2; v3 = w3;
-    }
-    for (; t < nk; ++t)  // fewer than four left
-      attend_key<HD, G>(ldg16(kp + (size_t)t * stride), ldg16(vp + (size_t)t * stride), q, o, m, l);
-    // combine the NGR groups
+    // combine the NGR groups: R threads per output, NGR / R groups each
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) {
       if (li == 0) {
@@ -635,47 +748,95 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos,
     }
     __syncthreads();
     float* part = a.part + (size_t)g * G * S * (HD + 2);
-    for (int e = tid; e < G * HD; e += kT) {
-      const int gg = e / HD, dim = e % HD;
+    {
+      const int c = tid % NOUT, r = tid / NOUT;  // output c, part r
+      const int gg = c / HD, dim = c % HD;
       float M = -INFINITY;
       for (int k = 0; k < NGR; ++k) M = fmaxf(M, sm_m[k * G + gg]);
       float Ls = 0.f, Os = 0.f;
-      if (M != -INFINITY) {
-        for (int k = 0; k < NGR; ++k) {
+      if (r < R && M != -INFINITY) {
+        for (int k = r * (NGR / R); k < (r + 1) * (NGR / R); ++k) {
           const float mk = sm_m[k * G + gg];
-          if (mk == -INFINITY) continue;
-          const float w = exp2f(mk - M);
+          const float w = mk == -INFINITY ? 0.f : exp2f(mk - M);
           Ls = fmaf(w, sm_l[k * G + gg], Ls);
           Os = fmaf(w, sm_o[(k * G + gg) * HD + dim], Os);
         }
       }
-      float* slot = part + ((size_t)gg * S + s) * (HD + 2);
-      stf_dev(slot + dim, Os);
-      if (dim == 0) {
-        stf_dev(slot + HD, M);
-        stf_dev(slot + HD + 1, Ls);
+      __syncthreads();
+      if (r < R) {
+        sm_r[r * NOUT + c] = Os;
+        if (dim == 0) sm_r[R * NOUT + r * G + gg] = Ls;
+      }
+      __syncthreads();
+      if (tid < NOUT) {
+        float Ot = 0.f, Lt = 0.f;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          Ot += sm_r[k * NOUT + c];
+          Lt += sm_r[R * NOUT + k * G + gg];
+        }
+        float* slot = part + ((size_t)gg * S + s) * (HD + 2);
+        stf_dev(slot + dim, Ot);
+        if (dim == 0) {
+          stf_dev(slot + HD, M);
+          stf_dev(slot + HD + 1, Lt);
+        }
       }
     }
     wg_publish();
     if (tid == 0) sm.flag = add_dev(a.sync + kSyncAttn + g, 1u) == (unsigned)(S - 1);
     __syncthreads();
     if (sm.flag) {
-      // last split of kv head g: merge the S partials of its G query heads
-      for (int e = tid; e < G * HD; e += kT) {
-        const int gg = e / HD, dim = e % HD;
-        const float* base = part + (size_t)gg * S * (HD + 2);
+      // last split of kv head g: merge the S partials of its G query heads.
+      // 1) all (max, sum) pairs at once
+      float* mm = sm_r;             // [G][S]
+      float* ww = sm_r + G * S;     // [G][S] weights, then [G] totals
+      for (int e = tid; e < G * S; e += kT) {
+        const int gg = e / S, k = e % S;
+        const float* sl = part + ((size_t)gg * S + k) * (HD + 2);
+        mm[e] = ldf_dev(sl + HD);
+        ww[e] = ldf_dev(sl + HD + 1);
+      }
+      __syncthreads();
+      if (tid < G) {
         float M = -INFINITY;
-        for (int k = 0; k < S; ++k) M = fmaxf(M, ldf_dev(base + (size_t)k * (HD + 2) + HD));
-        float Ls = 0.f, Os = 0.f;
+        for (int k = 0; k < S; ++k) M = fmaxf(M, mm[tid * S + k]);
+        float Lt = 0.f;
         for (int k = 0; k < S; ++k) {
-          const float* sl = base + (size_t)k * (HD + 2);
-          const float mk = ldf_dev(sl + HD);
-          if (mk == -INFINITY) continue;
-          const float w = exp2f(mk - M);
-          Ls = fmaf(w, ldf_dev(sl + HD + 1), Ls);
-          Os = fmaf(w, ldf_dev(sl + dim), Os);
+          const float w = mm[tid * S + k] == -INFINITY ? 0.f : exp2f(mm[tid * S + k] - M);
+          Lt = fmaf(w, ww[tid * S + k], Lt);
+          mm[tid * S + k] = w;  // reuse as the weight of split k
         }
-        stf_dev(a.o + (size_t)(g * G + gg) * HD + dim, Os / Ls);
+        ww[G * S + tid] = Lt;
+      }
+      __syncthreads();
+      // 2) R threads per output, each over every R-th split, loads first
+      const int c = tid % NOUT, r = tid / NOUT;
+      const int gg = c / HD, dim = c % HD;
+      float acc = 0.f;
+      if (r < R) {
+        const float* base = part + (size_t)gg * S * (HD + 2) + dim;
+        int k = r;
+        for (; k + 3 * R < S; k += 4 * R) {
+          const float x0 = ldf_dev(base + (size_t)k * (HD + 2));
+          const float x1 = ldf_dev(base + (size_t)(k + R) * (HD + 2));
+          const float x2 = ldf_dev(base + (size_t)(k + 2 * R) * (HD + 2));
+          const float x3 = ldf_dev(base + (size_t)(k + 3 * R) * (HD + 2));
+          acc = fmaf(mm[gg * S + k], x0, acc);
+          acc = fmaf(mm[gg * S + k + R], x1, acc);
+          acc = fmaf(mm[gg * S + k + 2 * R], x2, acc);
+          acc = fmaf(mm[gg * S + k + 3 * R], x3, acc);
+        }
+        for (; k < S; k += R) acc = fmaf(mm[gg * S + k], ldf_dev(base + (size_t)k * (HD + 2)), acc);
+      }
+      float* red = sm_o;  // [R][NOUT]; the group outputs are no longer needed
+      if (r < R) red[r * NOUT + c] = acc;
+      __syncthreads();
+      if (tid < NOUT) {
+        float ot = 0.f;
+#pragma unroll
+        for (int k = 0; k < R; ++k) ot += red[k * NOUT + c];
+        stf_dev(a.o + (size_t)(g * G + gg) * HD + dim, ot / ww[G * S + gg]);
       }
       if (tid == 0) st_dev(a.sync + kSyncAttn + g, 0u);
     }
@@ -692,46 +853,40 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   // advances it for the next launch once that barrier has passed
   const unsigned ep0 = ld_dev(a.sync + kSyncEpoch);
   unsigned k = 0;
-  uint4 A[kNLD], B[kNLD];
-  {
-    const GPhase P = make_phase<WFMT, K_QKV>(a, 0);
-    issue<WFMT, K_QKV, VQ, HD>(a, P, 0, A);
-  }
+  Bufs W;
+  prefetch<WFMT, HD, K_QKV, VQ>(a, 0, W);
+  auto none = [] {};
   for (int l = 0; l < a.L; ++l) {
     {
       const GPhase P = make_phase<WFMT, K_QKV>(a, l);
-      gemv_phase<WFMT, HD, K_QKV, VQ, -1, 1>(a, P, l, l, pos, token, A, B, lds, sm);
+      gemv_phase<WFMT, HD, K_QKV, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
     }
-    grid_sync(a, ep0, ++k);
+    grid_sync(a, ep0, ++k, none);
     if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0)
       st_dev(a.sync + kSyncEpoch, ep0 + 5u * (unsigned)a.L);
     attn_phase<HD, G>(a, l, pos, lds, sm);
-    {
-      const GPhase N = make_phase<WFMT, K_O>(a, l);
-      issue<WFMT, K_O, VQ, HD>(a, N, 0, A);
-    }
-    grid_sync(a, ep0, ++k);
+    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_O, VQ>(a, l, W); });
     {
       const GPhase P = make_phase<WFMT, K_O>(a, l);
-      gemv_phase<WFMT, HD, K_O, VQ, K_GU, VQ>(a, P, l, l, pos, token, A, B, lds, sm);
+      gemv_phase<WFMT, HD, K_O, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
     }
-    grid_sync(a, ep0, ++k);
+    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_GU, VQ>(a, l, W); });
     {
       const GPhase P = make_phase<WFMT, K_GU>(a, l);
-      gemv_phase<WFMT, HD, K_GU, VQ, K_DOWN, VD>(a, P, l, l, pos, token, A, B, lds, sm);
+      gemv_phase<WFMT, HD, K_GU, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
     }
-    grid_sync(a, ep0, ++k);
+    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_DOWN, VD>(a, l, W); });
     {
       const GPhase P = make_phase<WFMT, K_DOWN>(a, l);
-      if (l + 1 < a.L)
-        gemv_phase<WFMT, HD, K_DOWN, VD, K_QKV, VQ>(a, P, l, l + 1, pos, token, A, B, lds, sm);
-      else
-        gemv_phase<WFMT, HD, K_DOWN, VD, K_LM, VQ>(a, P, l, l + 1, pos, token, A, B, lds, sm);
+      gemv_phase<WFMT, HD, K_DOWN, VD>(a, P, l, pos, token, W, lds, sm, k + 1);
     }
-    grid_sync(a, ep0, ++k);
+    if (l + 1 < a.L)
+      grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_QKV, VQ>(a, l + 1, W); });
+    else
+      grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_LM, VQ>(a, l + 1, W); });
   }
   const GPhase P = make_phase<WFMT, K_LM>(a, a.L);
-  gemv_phase<WFMT, HD, K_LM, VQ, -1, 1>(a, P, a.L, a.L, pos, token, A, B, lds, sm);
+  gemv_phase<WFMT, HD, K_LM, VQ>(a, P, a.L, pos, token, W, lds, sm, 0u);
 }
 
 template <int WFMT, int HD, int G, int VQ, int VD>
@@ -791,7 +946,12 @@ bool aio_step_kernel_supports(const aio_config& c) {
 size_t aio_step_kernel_lds(const aio_config& c, int blocks) {
   const int G = c.n_heads / c.n_kv_heads;
   const int ngr = kT / (c.head_dim / 8);
-  const size_t attn = (size_t)ngr * G * (c.head_dim + 2) * 4;
+  const int nout = G * c.head_dim;
+  const int r = kT / nout > 0 ? kT / nout : 1;
+  const int S = AIO_STEP_MAX_BLOCKS / c.n_kv_heads > 0 ? AIO_STEP_MAX_BLOCKS / c.n_kv_heads : 1;
+  // group state + [R][NOUT] partials (+ R * G sums) or the merge's 2 G S + G
+  const size_t scratch = std::max((size_t)r * nout + (size_t)r * G, (size_t)2 * G * S + G);
+  const size_t attn = ((size_t)ngr * G * (c.head_dim + 2) + scratch) * 4;
   auto red = [&](int units, int rpu) { return (size_t)((units + blocks - 1) / blocks) * rpu * kW * 4; };
   size_t gemv = red((c.n_heads + 2 * c.n_kv_heads) * c.head_dim / 4, 4);
   gemv = std::max(gemv, red(c.d_model, 1));
@@ -801,7 +961,8 @@ size_t aio_step_kernel_lds(const aio_config& c, int blocks) {
 }
 
 hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* tokens_out,
-                                  unsigned long long* trace) {
+                                  unsigned long long* trace, unsigned long long* bar_arrive,
+                                  unsigned long long* bar_leave) {
   const aio_config& c = m.cfg;
   MegaArgs a{};
   a.layers = m.mega_layers;
@@ -820,6 +981,9 @@ hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* to
   a.logits = logits;
   a.tokens_out = tokens_out;
   a.trace = trace;
+  a.bar_arrive = bar_arrive;
+  a.bar_leave = bar_leave;
+  a.detail = bar_leave ? bar_leave + (size_t)(5 * c.n_layers + 1) * m.mega_blocks : nullptr;
   a.L = c.n_layers;
   a.d = c.d_model;
   a.H = c.n_heads;
