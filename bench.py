@@ -10,8 +10,12 @@ Inputs (weights, KV cache) are resident in HBM before the timed region; the
 loop is device-resident (captured graph replayed per step, argmax feeding the
 next token on the device).
 
-Prints one JSON line.  The HBM roofline figure is for the dominant kernel
-(the fused gate/up GEMV), timed with HIP events on the model's stream; the
+Prints one JSON line.  The HBM roofline figure is for the dominant kernel --
+the persistent step kernel, which is the whole step (or, on the per-operation
+path, the fused gate/up GEMV) -- timed with HIP events on the model's stream;
+its `traffic` is the HBM bytes per launch that rocprofv3's FETCH_SIZE and
+WRITE_SIZE counters read for this kernel (calibrated against a plain copy),
+reported only while the kernel's device sources are the ones measured.  The
 CPU baseline is the oracle, timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -44,6 +48,48 @@ def workload_name(cfg) -> str:
                                         cfg.wfmt, cfg.prompt_len))
 
 
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_step_7b_2k_traffic.json")
+
+
+def measured_traffic(config: str, kernel_used: bool):
+    """HBM bytes per step-kernel launch from the committed counter record, or
+    None when the workload differs or the kernel's sources changed since."""
+    import hashlib
+    if config != "7b" or not kernel_used or not os.path.exists(TRAFFIC_RECORD):
+        return None
+    rec = json.load(open(TRAFFIC_RECORD))
+    h = hashlib.sha256()
+    for f in rec["device_sources"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
+    return int(rec["traffic_bytes_per_launch"])
+
+
+def calibrate_copy(nbytes: int) -> int:
+    """A plain copy of a known number of bytes: read nbytes, write nbytes.
+    Profiled with the same HBM counters as the decode step, it gives the
+    factor between counter readings and bytes actually moved."""
+    import torch
+    if not torch.cuda.is_available():
+        print("--calibrate-copy needs a GPU", file=sys.stderr)
+        return 2
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    reps = 5
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    print(json.dumps({"copy_bytes": nbytes, "launches": reps + 1, "read_plus_write_gbs":
+                      round(2 * nbytes / dt / 1e9, 1)}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -54,7 +100,12 @@ def main() -> int:
                     help="wall-clock budget of the oracle's CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="instead of the decode bench, run a plain device-to-device copy of "
+                         "BYTES (the reference kernel for HBM counter calibration) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        return calibrate_copy(args.calibrate_copy)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -178,7 +229,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(args.config, dm.uses_step_kernel),
             "bytes_per_launch": int(k_bytes),
             "avg_launch_us": round(k_us, 2),
         },

@@ -177,8 +177,9 @@ int aio_argmax(aio_model* m, const float* logits_dev, int32_t rows, int32_t n, i
 
 /* Device-resident greedy decoding for timing: consume `token` at `pos`, then
  * feed each step's argmax as the next token, for n_steps steps, with no host
- * round trip inside the loop (the step is replayed from a captured HIP graph
- * when AIO_GRAPH is not "0").  tokens_dev (int32 [n_steps]) receives the
+ * round trip inside the loop (the persistent step kernel reads the token and
+ * position from device state and advances them; the per-operation path
+ * replays a captured HIP graph unless AIO_GRAPH is "0").  tokens_dev (int32 [n_steps]) receives the
  * argmax of every step; logits_dev (fp32 [vocab]) holds the last step's
  * logits.  AIO_ERANGE if pos + n_steps > max_ctx. */
 int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
@@ -187,9 +188,10 @@ int aio_decode_greedy(aio_model* m, int32_t token, int32_t pos, int32_t n_steps,
 /* Profiling: one aio_decode_step with a HIP event recorded on the model's
  * stream before the first kernel and after every kernel, then a wait for the
  * last event.  kernel_ms (host, max_kernels floats) receives each kernel's
- * event-to-event time in launch order -- per layer: qkv, attention,
- * split merge, o-projection, gate/up, down; then the LM head -- and
- * *n_kernels the count written.  Synchronises; not for the timed loop. */
+ * event-to-event time in launch order -- one entry for the persistent step
+ * kernel, else per layer: qkv, attention, split merge, o-projection,
+ * gate/up, down; then the LM head -- and *n_kernels the count written.
+ * Synchronises; not for the timed loop. */
 int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
                      float* kernel_ms, int32_t max_kernels, int32_t* n_kernels);
 

@@ -60,6 +60,7 @@ struct aio_model {
   bool use_graph;
   // persistent step kernel (one cooperative launch per decode step)
   bool use_mega;
+  bool mega_coop;  // cooperative launch (default); plain launch when AIO_STEP_LAUNCH=plain
   int mega_blocks;
   MegaLayer* mega_layers;          // library-owned device table [n_layers]
   unsigned long long* mega_trace;  // library-owned, allocated on first trace

@@ -199,6 +199,8 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
                 prop.cooperativeLaunch;
   m->mega_blocks = prop.multiProcessorCount < AIO_STEP_MAX_BLOCKS ? prop.multiProcessorCount
                                                                    : AIO_STEP_MAX_BLOCKS;
+  const char* sl = getenv("AIO_STEP_LAUNCH");
+  m->mega_coop = !(sl && strcmp(sl, "plain") == 0);
 
   // RoPE table: cos/sin of pos * base^(-2i/hd), angles in double, stored fp32.
   const int half = cfg->head_dim / 2;

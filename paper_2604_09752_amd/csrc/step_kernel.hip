@@ -889,34 +889,40 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   gemv_phase<WFMT, HD, K_LM, VQ>(a, P, a.L, pos, token, W, lds, sm, 0u);
 }
 
+// The grid is one workgroup per CU and a CU holds at most one (registers
+// and LDS), so all workgroups are resident together.  The cooperative
+// launch states that requirement to the runtime, which refuses the launch
+// if it cannot be met; a plain launch of the same grid relies on the GPU
+// running nothing else (every barrier wait is bounded either way).
 template <int WFMT, int HD, int G, int VQ, int VD>
-hipError_t launch_t(const MegaArgs& a, int blocks, size_t lds, hipStream_t s) {
+hipError_t launch_t(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, bool coop) {
   void* args[] = {(void*)&a};
+  const void* fn = (const void*)k_step<WFMT, HD, G, VQ, VD>;
   if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_step<WFMT, HD, G, VQ, VD>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  return hipLaunchCooperativeKernel((const void*)k_step<WFMT, HD, G, VQ, VD>, dim3(blocks),
-                                    dim3(kT), args, (unsigned)lds, s);
+  if (coop) return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kT), args, (unsigned)lds, s);
+  return hipLaunchKernel(fn, dim3(blocks), dim3(kT), args, lds, s);
 }
 
 template <int WFMT, int HD, int G>
-hipError_t launch_vd(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, int vd) {
+hipError_t launch_vd(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, int vd, bool coop) {
   switch (vd) {
-    case 1: return launch_t<WFMT, HD, G, 1, 1>(a, blocks, lds, s);
-    case 2: return launch_t<WFMT, HD, G, 1, 2>(a, blocks, lds, s);
-    case 3: return launch_t<WFMT, HD, G, 1, 3>(a, blocks, lds, s);
+    case 1: return launch_t<WFMT, HD, G, 1, 1>(a, blocks, lds, s, coop);
+    case 2: return launch_t<WFMT, HD, G, 1, 2>(a, blocks, lds, s, coop);
+    case 3: return launch_t<WFMT, HD, G, 1, 3>(a, blocks, lds, s, coop);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int WFMT, int HD>
-hipError_t launch_g(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, int G, int vd) {
+hipError_t launch_g(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, int G, int vd,
+                    bool coop) {
   switch (G) {
-    case 1: return launch_vd<WFMT, HD, 1>(a, blocks, lds, s, vd);
-    case 2: return launch_vd<WFMT, HD, 2>(a, blocks, lds, s, vd);
-    case 4: return launch_vd<WFMT, HD, 4>(a, blocks, lds, s, vd);
+    case 1: return launch_vd<WFMT, HD, 1>(a, blocks, lds, s, vd, coop);
+    case 2: return launch_vd<WFMT, HD, 2>(a, blocks, lds, s, vd, coop);
+    case 4: return launch_vd<WFMT, HD, 4>(a, blocks, lds, s, vd, coop);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1001,11 +1007,11 @@ hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* to
   const int vd = aio_step_kernel_vpl(c, c.ffn_dim);
   hipError_t e;
   if (c.wfmt == AIO_WFMT_INT8)
-    e = c.head_dim == 128 ? launch_g<AIO_WFMT_INT8, 128>(a, blocks, lds, m.stream, G, vd)
-                          : launch_g<AIO_WFMT_INT8, 64>(a, blocks, lds, m.stream, G, vd);
+    e = c.head_dim == 128 ? launch_g<AIO_WFMT_INT8, 128>(a, blocks, lds, m.stream, G, vd, m.mega_coop)
+                          : launch_g<AIO_WFMT_INT8, 64>(a, blocks, lds, m.stream, G, vd, m.mega_coop);
   else
-    e = c.head_dim == 128 ? launch_g<AIO_WFMT_BF16, 128>(a, blocks, lds, m.stream, G, vd)
-                          : launch_g<AIO_WFMT_BF16, 64>(a, blocks, lds, m.stream, G, vd);
+    e = c.head_dim == 128 ? launch_g<AIO_WFMT_BF16, 128>(a, blocks, lds, m.stream, G, vd, m.mega_coop)
+                          : launch_g<AIO_WFMT_BF16, 64>(a, blocks, lds, m.stream, G, vd, m.mega_coop);
   aio_prof_mark(m);
   return e;
 }
