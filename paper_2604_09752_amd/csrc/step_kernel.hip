@@ -57,6 +57,7 @@ constexpr int kNLD = 8;          // 16-byte weight loads per lane per batch
 // prefetch delays every workgroup's view of the release.
 constexpr int kNBUF = 2;
 constexpr unsigned kSpinLimit = 1u << 17;  // ~0.1-0.2 s of polling
+
 // s_waitcnt immediate for vmcnt(0) with expcnt and lgkmcnt left at their
 // maximum (no wait): vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8].
 constexpr int kVmcnt0 = 0x0F70;
@@ -80,8 +81,14 @@ AIO_DEV unsigned add_dev(unsigned* p, unsigned v) {
 AIO_DEV float ldf_dev(const float* p) { return __uint_as_float(ld_dev((const unsigned*)p)); }
 AIO_DEV void stf_dev(float* p, float v) { st_dev((unsigned*)p, __float_as_uint(v)); }
 
-// Wait for this thread's stores, then for the whole workgroup.
+// Wait until this thread's stores have completed, then for the whole
+// workgroup; a flag or counter written after this is seen by other
+// workgroups only after the data.  The device-scope stores are acknowledged
+// once they are visible at device scope; the wait is explicit because a
+// workgroup-scope fence does not wait for global stores (the workgroup
+// shares one CU).
 AIO_DEV void wg_publish() {
+  __builtin_amdgcn_s_waitcnt(kVmcnt0);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
 }
@@ -580,13 +587,18 @@ AIO_DEV void gemv_phase(const MegaArgs& a, const GPhase& P, int layer, int pos, 
   // Branch-free body: a batch past the end is computed fully masked and its
   // refill is a masked dummy (cache-hit) load, so the compiler sees the same
   // loads in flight behind each buffer on every path.
-  for (int b = 0; b < nb; b += kNBUF) {
+  int b = 0;
+  for (; b + kNBUF < nb; b += kNBUF) {
 #pragma unroll
     for (int j = 0; j < kNBUF; ++j) {
       compute<WFMT, KIND, VPL>(P, b + j, W.b[j], h, red, T);
       issue<WFMT, KIND, VPL, HD>(a, P, b + j + kNBUF, W.b[j], T);
     }
   }
+  // last round: no refills, so that nothing is in flight when the phase's
+  // outputs are published (the release waits for every outstanding load)
+#pragma unroll
+  for (int j = 0; j < kNBUF; ++j) compute<WFMT, KIND, VPL>(P, b + j, W.b[j], h, red, T);
   __syncthreads();
   if (a.detail && T.tid == 0) a.detail[((size_t)kb * gridDim.x + blockIdx.x) * 2 + 1] = wall_clock64();
   epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, T);
