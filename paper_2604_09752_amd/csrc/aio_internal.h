@@ -32,7 +32,15 @@ struct WsLayout {
   size_t act;      // bf16 [2][32][KA]        split activations for the verify GEMM
   size_t amax;     // int32 [MV]              argmax scratch
   size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters
-  size_t mega_part;  // fp32 [H][S_mega][hd+2] step-kernel split partials
+  // step-kernel exchange buffers (tagged words), mega_xa .. mega_end zeroed at load
+  size_t mega_xa;    // [d]
+  size_t mega_xb;    // [d]
+  size_t mega_q;     // [H*hd]
+  size_t mega_kvn;   // [2][Hkv][hd]
+  size_t mega_o;     // [H*hd]
+  size_t mega_m;     // [F]
+  size_t mega_part;  // [H][S_mega][hd+2] split partials
+  size_t mega_end;
   size_t total;
   int splits;      // S, split-KV partitions per head
   int mega_splits; // S_mega, split-KV partitions per kv head in the step kernel

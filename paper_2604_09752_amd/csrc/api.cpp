@@ -67,8 +67,15 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
   L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
   if (L.mega_splits < 1) L.mega_splits = 1;
+  L.mega_xa = off; off = align256(off + d * 4);
+  L.mega_xb = off; off = align256(off + d * 4);
+  L.mega_q = off; off = align256(off + Hd * 4);
+  L.mega_kvn = off; off = align256(off + 2 * (size_t)c.n_kv_heads * c.head_dim * 4);
+  L.mega_o = off; off = align256(off + Hd * 4);
+  L.mega_m = off; off = align256(off + F * 4);
   L.mega_part = off;
   off = align256(off + (size_t)c.n_heads * (size_t)L.mega_splits * ((size_t)c.head_dim + 2) * 4);
+  L.mega_end = off;
   L.total = off;
   return L;
 }
@@ -238,6 +245,8 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
       e = hipMemcpy(m->mega_layers, tab.data(), tab.size() * sizeof(MegaLayer),
                     hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
+    if (e == hipSuccess)
+      e = hipMemset(m->ws + m->lay.mega_xa, 0, m->lay.mega_end - m->lay.mega_xa);
   }
   if (e != hipSuccess) {
     if (m->rope) (void)hipFree(m->rope);

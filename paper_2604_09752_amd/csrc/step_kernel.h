@@ -22,11 +22,8 @@ struct MegaLayer {
 
 // Words of the synchronisation region (uint32, zeroed at load).
 enum {
-  kSyncFlags = 0,        // [1024] barrier arrival epochs, one per workgroup
-  kSyncRelease = 1024,   // barrier release epoch
   kSyncEpoch = 1040,     // epoch base carried from one launch to the next
   kSyncErr = 1056,       // set when a bounded wait gives up
-  kSyncAttn = 1088,      // [1024] split counters per kv head
   kSyncAmaxCount = 2112, // argmax arrival counter
   kSyncAmax = 2176,      // [1024][2] per-workgroup (value, index)
   kSyncWords = 4224
@@ -43,18 +40,22 @@ struct MegaArgs {
   const uint16_t* s_lm;
   const float2* rope;
   aio_state* st;
-  float* x;        // [d]     residual
-  float* q;        // [H*hd]  rotated queries
-  float* o;        // [H*hd]  attention output
-  float* m;        // [F]     SwiGLU output
-  float* part;     // [H][S][hd + 2] split partials (output, max, sum)
+  // Buffers exchanged between workgroups, every word tagged with the version
+  // of the phase that wrote it (zeroed at load: version 0, never expected).
+  unsigned* xa;    // [d]            residual after the attention block
+  unsigned* xb;    // [d]            residual after the MLP block
+  unsigned* q;     // [H*hd]         rotated queries
+  unsigned* kvn;   // [2][Hkv][hd]   new K and V rows, bf16 << 16 | version
+  unsigned* o;     // [H*hd]         attention output
+  unsigned* m;     // [F]            SwiGLU output
+  unsigned* part;  // [H][S][hd + 2] split partials (output, max, sum)
   unsigned* sync;  // kSyncWords
   float* logits;   // [V]
   int32_t* tokens_out;
-  unsigned long long* trace;  // optional: barrier exit times (workgroup 0), [5 L + 1]
-  unsigned long long* bar_arrive;  // optional: [5 L + 1][blocks] arrival times
-  unsigned long long* bar_leave;   // optional: [5 L + 1][blocks] exit times
-  unsigned long long* detail;      // optional: [5 L + 1][blocks][2] input-ready, loop-done
+  unsigned long long* trace;       // optional: [5 L + 2] workgroup 0's publish time of each phase
+  unsigned long long* bar_arrive;  // optional: [5 L + 1][blocks] publish time of phase k
+  unsigned long long* bar_leave;   // optional: [5 L + 1][blocks] time the inputs of phase k + 1 were in
+  unsigned long long* detail;      // optional: [5 L + 1][blocks][2] loop start and end of phase k
   int L, d, H, Hkv, hd, F, V, max_ctx, S;
   float eps, scale_log2;
 };

@@ -5,17 +5,18 @@
 // five dependent matrix-vector products and an attention.  Launched as
 // separate kernels, each link pays a dispatch ramp, a prologue and a tail
 // (several microseconds each, ~190 links per 7B token).  Here one workgroup
-// per CU (512 threads, 8 waves) walks all phases of all layers, separated by
-// grid barriers, and issues the first weight loads of the next phase before
-// each barrier so HBM keeps streaming while the grid synchronises.
+// per CU (512 threads, 8 waves) walks all phases of all layers, and issues
+// the first weight loads of each phase as soon as it has finished the one
+// before, so HBM keeps streaming while the workgroup waits for its inputs.
 //
-// Phases per layer, each followed by a grid barrier:
+// Phases per layer (phase index k = 5 l + 1 .. 5 l + 5):
 //   QKV   RMSNorm(x) -> q, k, v rows -> RoPE; q stored, k/v appended (bf16)
-//   ATTN  split-KV flash-decode per (kv head, split); the last split to
-//         finish for a kv head merges all splits (log-sum-exp) into o
-//   O     x += W_o o
-//   GU    RMSNorm(x) -> m = silu(W_gate h) * (W_up h)
-//   DOWN  x += W_down m
+//   ATTN  split-KV flash-decode per (kv head, split) over the cached keys;
+//         the last split of a kv head also takes the new key, and then
+//         merges the S partials of its head (log-sum-exp) into o
+//   O     x' = x + W_o o
+//   GU    RMSNorm(x') -> m = silu(W_gate h) * (W_up h)
+//   DOWN  x = x' + W_down m
 // then LM head (RMSNorm(x) -> logits) with the greedy argmax fused: each
 // workgroup reduces its rows and the last one to finish reduces the
 // workgroup results, writes the token and advances the position.
@@ -27,17 +28,34 @@
 // every wait for a buffer names only the loads issued before it (the loops
 // are branch-free and nothing else is loaded inside them).
 //
-// Coherence: the 8 XCDs have separate L2 caches that are not kept coherent
-// with each other, and a device-scope fence (L2 write-back + invalidate)
-// costs 15-20 us.  So every value one workgroup produces for another (x, q,
-// o, m, split partials, the new K/V row, barrier flags) is written with
-// device-scope stores and read with device-scope loads (both bypass the
-// non-coherent L2); a workgroup-scope fence then only has to wait for its own
-// stores to complete.  Weights and older KV rows are read-only in the step
-// and use ordinary loads.
+// Synchronisation without grid barriers: every value one workgroup produces
+// for another carries its own readiness.  An fp32 value is stored with the
+// 3-bit version (epoch base + phase index) mod 8 in its lowest mantissa bits
+// (the value truncated to 20 mantissa bits: a relative change below 2^-20);
+// the new K/V row goes out as bf16 in the high half of a word whose low bits
+// hold the version.  A consumer loads its slice of a buffer and reloads each
+// word whose version is not the one it expects.  A stale word holds the
+// buffer's previous use, five phases earlier, whose version differs mod 8.
+// A phase therefore starts one memory round trip after the words it needs
+// are stored, instead of after a flag store, a gather, a release and a
+// second load; and its first poll is issued right behind the phase's
+// prefetched weights, so it usually returns together with them.
 //
-// Every wait is a bounded spin: if a barrier never completes the kernel sets
-// an error word and runs to its end instead of hanging.
+// Reuse of a buffer needs no barrier either: every phase waits for all the
+// outputs of the phase before it (attention: every q row of its head, the
+// merge: every split of its head, O: all of o), so a producer reaches its
+// next write of a buffer, five phases on, only after every reader of the
+// previous contents has consumed them.  A workgroup with no rows in a phase
+// reads nothing in it.
+//
+// Coherence: the 8 XCDs have separate L2 caches that are not kept coherent
+// with each other, so every value exchanged between workgroups is written
+// with device-scope stores and read with device-scope loads, which bypass
+// the non-coherent L2.  Weights, norm gains and older KV rows are read-only
+// in the step and use ordinary loads.
+//
+// Every wait is a bounded spin: if a value never arrives the kernel sets an
+// error word and runs to its end instead of hanging.
 #include <math.h>
 
 #include <algorithm>
@@ -51,16 +69,17 @@ namespace {
 constexpr int kT = 512;          // threads per workgroup
 constexpr int kW = kT / AIO_WAVE; // waves per workgroup
 constexpr int kNLD = 8;          // 16-byte weight loads per lane per batch
-// Batches in flight per wave (register buffers).  Three stream the loops
-// faster but lose overall: the barrier's polling loads are queued behind the
-// prefetched weight loads (vector memory returns in order), so a deeper
-// prefetch delays every workgroup's view of the release.
+// Batches in flight per wave (register buffers).  A deeper prefetch streams
+// the loops a little faster but delays the input poll queued behind it
+// (vector memory returns in order).
 constexpr int kNBUF = 2;
 constexpr unsigned kSpinLimit = 1u << 17;  // ~0.1-0.2 s of polling
 
 // s_waitcnt immediate for vmcnt(0) with expcnt and lgkmcnt left at their
 // maximum (no wait): vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8].
 constexpr int kVmcnt0 = 0x0F70;
+// Cache-policy operand of a buffer load: device scope (sc1).
+constexpr int kSC1 = 16;
 
 enum Kind { K_QKV = 0, K_O = 1, K_GU = 2, K_DOWN = 3, K_LM = 4 };
 
@@ -78,61 +97,119 @@ AIO_DEV void st_dev(unsigned* p, unsigned v) {
 AIO_DEV unsigned add_dev(unsigned* p, unsigned v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-AIO_DEV float ldf_dev(const float* p) { return __uint_as_float(ld_dev((const unsigned*)p)); }
-AIO_DEV void stf_dev(float* p, float v) { st_dev((unsigned*)p, __float_as_uint(v)); }
+
+// 16-byte device-scope load of words base[off .. off + 3].  `base` must be
+// the same for the whole wave (it becomes a buffer descriptor).
+AIO_DEV u32x4 ld16_dev(const unsigned* base, int off) {
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 0x7ffffff0, 0x00020000);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off * 4, 0, kSC1);
+}
+
+typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
+
+// 16-byte ordinary load through a global-address-space pointer (weights,
+// gains and K/V rows come from a table in memory, so the compiler cannot
+// infer the address space).
+AIO_DEV uint4 ldg16(const uint16_t* p) {
+  const u32x4 v = *(gl_u32x4*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 // Wait until this thread's stores have completed, then for the whole
-// workgroup; a flag or counter written after this is seen by other
-// workgroups only after the data.  The device-scope stores are acknowledged
-// once they are visible at device scope; the wait is explicit because a
-// workgroup-scope fence does not wait for global stores (the workgroup
-// shares one CU).
+// workgroup; a counter raised after this is seen by other workgroups only
+// after the data.  The wait is explicit because a workgroup-scope fence does
+// not wait for global stores (the workgroup shares one CU).
 AIO_DEV void wg_publish() {
   __builtin_amdgcn_s_waitcnt(kVmcnt0);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
 }
 
-// Bounded wait.  Once any wait has given up (the error word is set), every
-// later wait returns at its next check, so a broken barrier costs well under
-// a second instead of hanging the device.
-AIO_DEV void spin_ge(const MegaArgs& a, const unsigned* p, unsigned target) {
-  unsigned spins = 0;
-  while ((int)(ld_dev(p) - target) < 0) {
-    __builtin_amdgcn_s_sleep(1);
-    if ((++spins & 255u) == 0) {
-      if (ld_dev(a.sync + kSyncErr) != 0u) break;
-      if (spins > kSpinLimit) {
-        st_dev(a.sync + kSyncErr, 1u);
-        break;
-      }
+// ----------------------------------------------------------------- versions
+
+AIO_DEV unsigned ver_of(unsigned ep0, unsigned k) { return (ep0 + k) & 7u; }
+AIO_DEV unsigned tagf(float v, unsigned ver) { return (__float_as_uint(v) & ~7u) | ver; }
+AIO_DEV float untagf(unsigned w) { return __uint_as_float(w & ~7u); }
+AIO_DEV void st_tag(unsigned* p, float v, unsigned ver) { st_dev(p, tagf(v, ver)); }
+AIO_DEV bool tags_ok(const u32x4 v, unsigned ver) {
+  return ((v.x & 7u) == ver) & ((v.y & 7u) == ver) & ((v.z & 7u) == ver) & ((v.w & 7u) == ver);
+}
+
+// One step of a bounded wait.  Once any wait has given up (the error word is
+// set), every later wait stops at its next check, so a value that never
+// arrives costs well under a second instead of hanging the device.
+AIO_DEV bool spin_on(const MegaArgs& a, unsigned& spins) {
+  __builtin_amdgcn_s_sleep(2);
+  if ((++spins & 63u) == 0) {
+    if (ld_dev(a.sync + kSyncErr) != 0u) return false;
+    if (spins > kSpinLimit) {
+      st_dev(a.sync + kSyncErr, 1u);
+      return false;
     }
+  }
+  return true;
+}
+
+// Calls f(0) .. f(N - 1) with constant indices.  A plain unrolled loop is
+// not unrolled by the compiler once it sits inside a wait loop, and the
+// arrays it indexes then move to scratch memory.
+template <int I, int N>
+struct Unroll {
+  template <class F>
+  AIO_DEV static void run(F&& f) {
+    f(I);
+    Unroll<I + 1, N>::run(f);
+  }
+};
+template <int N>
+struct Unroll<N, N> {
+  template <class F>
+  AIO_DEV static void run(F&&) {}
+};
+
+// Wait until the loaded 16-byte words this thread needs carry version `ver`,
+// reloading only the stale ones.
+template <int N>
+AIO_DEV void await16(const MegaArgs& a, const unsigned* base, const int (&off)[N],
+                     const bool (&need)[N], u32x4 (&v)[N], unsigned ver) {
+  unsigned spins = 0;
+  for (;;) {
+    bool stale = false;
+    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+      stale |= need[i] && !tags_ok(v[i], ver);
+    });
+    if (!stale || !spin_on(a, spins)) break;
+    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+      if (need[i] && !tags_ok(v[i], ver)) v[i] = ld16_dev(base, off[i]);
+    });
   }
 }
 
-// Grid barrier: every workgroup raises its flag to `epoch`; workgroup 0
-// gathers all flags and raises the release word; everyone waits for it.
-// The release fence before the flag is an s_waitcnt on every outstanding
-// vector memory operation (loads included), so `prefetch` -- the first
-// weight loads of the next phase -- is issued only after the flag is up; it
-// then proceeds while the workgroup waits for the release.
-template <class F>
-AIO_DEV void grid_sync(const MegaArgs& a, unsigned ep0, unsigned k, F&& prefetch) {
-  const unsigned epoch = ep0 + k;
-  wg_publish();
-  const int tid = threadIdx.x;
-  if (a.bar_arrive && tid == 0) a.bar_arrive[(size_t)k * gridDim.x + blockIdx.x] = wall_clock64();
-  if (tid == 0) st_dev(a.sync + kSyncFlags + blockIdx.x, epoch);
-  prefetch();
-  if (blockIdx.x == 0) {
-    for (int i = tid; i < (int)gridDim.x; i += kT) spin_ge(a, a.sync + kSyncFlags + i, epoch);
-    __syncthreads();
-    if (tid == 0) st_dev(a.sync + kSyncRelease, epoch);
+// The same for single words.
+template <int N>
+AIO_DEV void await4(const MegaArgs& a, const unsigned* base, const int (&off)[N],
+                    const bool (&need)[N], unsigned (&v)[N], unsigned ver) {
+  unsigned spins = 0;
+  for (;;) {
+    bool stale = false;
+    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+      stale |= need[i] && (v[i] & 7u) != ver;
+    });
+    if (!stale || !spin_on(a, spins)) break;
+    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+      if (need[i] && (v[i] & 7u) != ver) v[i] = ld_dev(base + off[i]);
+    });
   }
-  if (tid == 0) spin_ge(a, a.sync + kSyncRelease, epoch);
-  __syncthreads();
-  if (a.trace && blockIdx.x == 0 && tid == 0) a.trace[k] = wall_clock64();
-  if (a.bar_leave && tid == 0) a.bar_leave[(size_t)k * gridDim.x + blockIdx.x] = wall_clock64();
+}
+
+// Optional timing records (profiling aids; null in normal runs).
+AIO_DEV void stamp(unsigned long long* arr, unsigned k) {
+  if (arr && threadIdx.x == 0) arr[(size_t)k * gridDim.x + blockIdx.x] = wall_clock64();
+}
+AIO_DEV void stamp_detail(const MegaArgs& a, unsigned k, int col) {
+  if (a.detail && threadIdx.x == 0)
+    a.detail[((size_t)k * gridDim.x + blockIdx.x) * 2 + col] = wall_clock64();
 }
 
 // ------------------------------------------------------------- matrix phase
@@ -146,9 +223,6 @@ typedef __attribute__((address_space(4))) const MegaLayer CMegaLayer;
 AIO_DEV const CMegaLayer* layer_at(const MegaArgs& a, int layer) {
   return (const CMegaLayer*)(a.layers + layer);
 }
-
-
-typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
 
 // Streaming 16-byte weight load through a global-address-space pointer.
 AIO_DEV uint4 ldg_stream(const void* p) {
@@ -361,58 +435,107 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
 
 // This lane's slice of the phase input, normalised when the phase starts
 // with an RMSNorm.  The slice of wave w, vector v is elements
-// [(w * nvw + v * 64 + lane) * EPV, +EPV).
+// [(w * nvw + v * 64 + lane) * EPV, +EPV).  The norm gains are requested
+// first (they do not depend on other workgroups), then the input words,
+// which are polled until they carry version `ver`.
 template <int WFMT, int KIND, int VPL>
-AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token,
+AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token, unsigned ver,
                         float (&h)[VPL][epv<WFMT>()], float* red8, const Thr& T) {
-  constexpr int E = epv<WFMT>();
+  constexpr int E = epv<WFMT>(), NQ = E / 4, NG = E / 8;
+  constexpr bool NORM = KIND == K_QKV || KIND == K_GU || KIND == K_LM;
   const int lane = T.lane, wave = T.wave;
-  const float* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : a.x);
-  const bool emb = KIND == K_QKV && layer == 0;
-  float ss = 0.f;
-#pragma unroll
-  for (int v = 0; v < VPL; ++v) {
-    const int vi = v * AIO_WAVE + lane;
-    const int e0 = (wave * P.nvw + vi) * E;
-#pragma unroll
-    for (int i = 0; i < E; ++i) h[v][i] = 0.f;
-    if (vi < P.nvw) {
-      if (emb) {
-        const uint16_t* er = a.embed + (size_t)token * a.d + e0;
-#pragma unroll
-        for (int i = 0; i < E; ++i) h[v][i] = bf16_to_f32(er[i]);
-        if (blockIdx.x == 0) {
-#pragma unroll
-          for (int i = 0; i < E; ++i) stf_dev(a.x + e0 + i, h[v][i]);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < E; ++i) h[v][i] = ldf_dev(src + e0 + i);
-      }
-#pragma unroll
-      for (int i = 0; i < E; ++i) ss = fmaf(h[v][i], h[v][i], ss);
-    }
-  }
-  if (KIND == K_QKV || KIND == K_GU || KIND == K_LM) {
-    ss = wave_sum(ss);
-    if (lane == 0) red8[wave] = ss;
-    __syncthreads();
-    float tot = 0.f;
-#pragma unroll
-    for (int w = 0; w < kW; ++w) tot += red8[w];
-    __syncthreads();  // red8 is reused by the next phase
-    const float inv = rsqrtf(tot / (float)P.K + a.eps);
+  const bool any = P.u1 > P.u0;  // a workgroup with no rows reads nothing
+  uint4 gw[VPL][NG];
+  if constexpr (NORM) {
     const CMegaLayer* L = layer_at(a, layer < a.L ? layer : 0);
     const uint16_t* g = KIND == K_QKV ? L->attn_norm : (KIND == K_GU ? L->ffn_norm : a.final_norm);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
       const int vi = v * AIO_WAVE + lane;
-      if (vi < P.nvw) {
-        const int e0 = (wave * P.nvw + vi) * E;
+      const int e0 = (wave * P.nvw + (vi < P.nvw ? vi : 0)) * E;
 #pragma unroll
-        for (int i = 0; i < E; ++i) h[v][i] = h[v][i] * inv * bf16_to_f32(g[e0 + i]);
+      for (int j = 0; j < NG; ++j) gw[v][j] = ldg16(g + e0 + 8 * j);
+    }
+  }
+  if (KIND == K_QKV && layer == 0) {
+    const uint16_t* er = a.embed + (size_t)token * a.d;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const int vi = v * AIO_WAVE + lane;
+      const bool ok = vi < P.nvw;
+      const int e0 = (wave * P.nvw + (ok ? vi : 0)) * E;
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        const uint4 b = ldg16(er + e0 + 8 * j);
+        const uint32_t w[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          h[v][8 * j + 2 * i] = ok ? bf16_lo(w[i]) : 0.f;
+          h[v][8 * j + 2 * i + 1] = ok ? bf16_hi(w[i]) : 0.f;
+        }
       }
     }
+  } else {
+    const unsigned* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : (KIND == K_GU ? a.xa : a.xb));
+    int off[VPL * NQ];
+    bool need[VPL * NQ];
+    u32x4 w[VPL * NQ];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const int vi = v * AIO_WAVE + lane;
+      const bool ok = vi < P.nvw;
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) {
+        off[v * NQ + j] = (wave * P.nvw + (ok ? vi : 0)) * E + 4 * j;
+        need[v * NQ + j] = any && ok;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPL * NQ; ++i) w[i] = ld16_dev(src, off[i]);
+    await16(a, src, off, need, w, ver);
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) {
+        const u32x4 x = w[v * NQ + j];
+        const bool ok = need[v * NQ + j];
+        h[v][4 * j + 0] = ok ? untagf(x.x) : 0.f;
+        h[v][4 * j + 1] = ok ? untagf(x.y) : 0.f;
+        h[v][4 * j + 2] = ok ? untagf(x.z) : 0.f;
+        h[v][4 * j + 3] = ok ? untagf(x.w) : 0.f;
+      }
+    }
+  }
+  if constexpr (NORM) {
+    float ss = 0.f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) ss = fmaf(h[v][i], h[v][i], ss);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) red8[wave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int w8 = 0; w8 < kW; ++w8) tot += red8[w8];
+    __syncthreads();  // red8 is reused by the next phase
+    const float inv = rsqrtf(tot / (float)P.K + a.eps);
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        const uint32_t g4[4] = {gw[v][j].x, gw[v][j].y, gw[v][j].z, gw[v][j].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          h[v][8 * j + 2 * i] = h[v][8 * j + 2 * i] * inv * bf16_lo(g4[i]);
+          h[v][8 * j + 2 * i + 1] = h[v][8 * j + 2 * i + 1] * inv * bf16_hi(g4[i]);
+        }
+      }
+    }
+  } else {
+    // every wave is past the previous phase's reads of the LDS partials
+    __syncthreads();
   }
 }
 
@@ -448,11 +571,22 @@ struct Smem {
   unsigned flag;
 };
 
+// Residual row u before a phase that adds to it: the embedding row at the
+// first O projection, else this workgroup's own output of two phases back
+// (O reads the DOWN output, DOWN reads the O output; same rows, same
+// thread, so no wait).
+template <int KIND>
+AIO_DEV float resid(const MegaArgs& a, int layer, int token, int u) {
+  if (KIND == K_O && layer == 0) return bf16_to_f32(a.embed[(size_t)token * a.d + u]);
+  return untagf(ld_dev((KIND == K_O ? a.xb : a.xa) + u));
+}
+
 // Epilogue of a matrix phase: sum the kW wave partials of each row, then the
-// phase-specific output.
+// phase-specific output, stored with version `vo`.
 template <int WFMT, int KIND>
-AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, const float* red,
-                      Smem& sm, float xpre, const Thr& T) {
+AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, int token,
+                      const float* red, Smem& sm, float xpre, const Thr& T, unsigned vo,
+                      unsigned ep0) {
   constexpr int RPU = rpu_of<KIND>();
   const int nu = P.u1 - P.u0;
   const int tid = T.tid;
@@ -493,17 +627,24 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         }
       }
       if (sec == 0) {
-        stf_dev(a.q + rlo, y[0]);
-        stf_dev(a.q + rlo + 1, y[1]);
-        stf_dev(a.q + rlo + half, y[2]);
-        stf_dev(a.q + rlo + half + 1, y[3]);
+        st_tag(a.q + rlo, y[0], vo);
+        st_tag(a.q + rlo + 1, y[1], vo);
+        st_tag(a.q + rlo + half, y[2], vo);
+        st_tag(a.q + rlo + half + 1, y[3], vo);
       } else {
         const int g = rlo / a.hd, ii = rlo % a.hd;
         const CMegaLayer* L = layer_at(a, layer);
         uint16_t* c = (sec == 1 ? L->kc : L->vc) + ((size_t)g * a.max_ctx + pos) * a.hd;
-        st_dev((unsigned*)(c + ii), (unsigned)f32_to_bf16(y[0]) | ((unsigned)f32_to_bf16(y[1]) << 16));
-        st_dev((unsigned*)(c + ii + half),
-               (unsigned)f32_to_bf16(y[2]) | ((unsigned)f32_to_bf16(y[3]) << 16));
+        const unsigned b0 = f32_to_bf16(y[0]), b1 = f32_to_bf16(y[1]);
+        const unsigned b2 = f32_to_bf16(y[2]), b3 = f32_to_bf16(y[3]);
+        st_dev((unsigned*)(c + ii), b0 | (b1 << 16));
+        st_dev((unsigned*)(c + ii + half), b2 | (b3 << 16));
+        // the same bf16 values, tagged, for this step's attention
+        unsigned* n = a.kvn + ((size_t)(sec - 1) * a.Hkv + g) * a.hd + ii;
+        st_dev(n, (b0 << 16) | vo);
+        st_dev(n + 1, (b1 << 16) | vo);
+        st_dev(n + half, (b2 << 16) | vo);
+        st_dev(n + half + 1, (b3 << 16) | vo);
       }
     } else if constexpr (KIND == K_GU) {
       float g = y[0], up = y[1];
@@ -511,7 +652,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         g *= fp16_to_f32(P.s0[u]);
         up *= fp16_to_f32(P.s1[u]);
       }
-      stf_dev(a.m + u, g / (1.f + expf(-g)) * up);
+      st_tag(a.m + u, g / (1.f + expf(-g)) * up, vo);
     } else {
       float yy = y[0];
       if constexpr (WFMT == AIO_WFMT_INT8) yy *= fp16_to_f32(P.s0[u]);
@@ -519,8 +660,8 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         a.logits[u] = yy;
         if (am_better(yy, u, bv, bi)) { bv = yy; bi = u; }
       } else {
-        const float xo = t == tid ? xpre : ldf_dev(a.x + u);
-        stf_dev(a.x + u, xo + yy);
+        const float xo = t == tid ? xpre : resid<KIND>(a, layer, token, u);
+        st_tag((KIND == K_O ? a.xa : a.xb) + u, xo + yy, vo);
       }
     }
   }
@@ -528,7 +669,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
     // fused greedy argmax: workgroup result, then the last workgroup reduces
     block_argmax(bv, bi, sm.sv, sm.si);
     if (tid == 0) {
-      stf_dev((float*)(a.sync + kSyncAmax + 2 * blockIdx.x), bv);
+      st_dev(a.sync + kSyncAmax + 2 * blockIdx.x, __float_as_uint(bv));
       st_dev(a.sync + kSyncAmax + 2 * blockIdx.x + 1, (unsigned)bi);
     }
     wg_publish();
@@ -538,7 +679,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
       float gv = -INFINITY;
       int gi = 0x7fffffff;
       for (int b = tid; b < (int)gridDim.x; b += kT) {
-        const float v = ldf_dev((const float*)(a.sync + kSyncAmax + 2 * b));
+        const float v = __uint_as_float(ld_dev(a.sync + kSyncAmax + 2 * b));
         const int i = (int)ld_dev(a.sync + kSyncAmax + 2 * b + 1);
         if (am_better(v, i, gv, gi)) { gv = v; gi = i; }
       }
@@ -551,6 +692,8 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         st->pos = pos + 1;
         st->step += 1;
         st_dev(a.sync + kSyncAmaxCount, 0u);
+        // every workgroup has read the epoch base: advance it for the next step
+        st_dev(a.sync + kSyncEpoch, ep0 + 5u * (unsigned)a.L);
       }
     }
   }
@@ -561,24 +704,27 @@ struct Bufs {
   uint4 b[kNBUF][kNLD];
 };
 
-// One matrix phase.  On entry buffer j holds (in flight) batch j of this
+// Matrix phase k.  On entry buffer j holds (in flight) batch j of this
 // phase; each buffer is refilled with the phase's batch kNBUF further on as
 // soon as it is consumed.
 template <int WFMT, int HD, int KIND, int VPL>
-AIO_DEV void gemv_phase(const MegaArgs& a, const GPhase& P, int layer, int pos, int token,
-                        Bufs& W, float* red, Smem& sm, unsigned kb) {
+AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& W, float* red,
+                        Smem& sm, unsigned ep0, unsigned k) {
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
+  const GPhase P = make_phase<WFMT, KIND>(a, layer);
   const int nb = (P.u1 - P.u0 + UB - 1) / UB;
+  const unsigned slot = KIND == K_LM ? 0u : k;  // timing slot
   const Thr T = thr();
   // residual rows this workgroup will update, fetched now to hide the trip
   float xpre = 0.f;
   if (KIND == K_O || KIND == K_DOWN) {
-    if (T.tid < P.u1 - P.u0) xpre = ldf_dev(a.x + P.u0 + T.tid);
+    if (T.tid < P.u1 - P.u0) xpre = resid<KIND>(a, layer, token, P.u0 + T.tid);
   }
   float h[VPL][epv<WFMT>()];
-  load_input<WFMT, KIND, VPL>(a, P, layer, token, h, sm.red8, T);
-  if (a.detail && T.tid == 0) a.detail[((size_t)kb * gridDim.x + blockIdx.x) * 2] = wall_clock64();
+  load_input<WFMT, KIND, VPL>(a, P, layer, token, ver_of(ep0, k - 1), h, sm.red8, T);
+  stamp(a.bar_leave, k - 1);
+  stamp_detail(a, slot, 0);
   // The input loads above were issued after this phase's first batches,
   // so waiting for them has waited for everything; say so explicitly
   // (vmcnt(0)), so that the loop below starts from a state in which only
@@ -595,13 +741,17 @@ AIO_DEV void gemv_phase(const MegaArgs& a, const GPhase& P, int layer, int pos, 
       issue<WFMT, KIND, VPL, HD>(a, P, b + j + kNBUF, W.b[j], T);
     }
   }
-  // last round: no refills, so that nothing is in flight when the phase's
-  // outputs are published (the release waits for every outstanding load)
+  // last round: no refills, so that nothing is queued ahead of the next
+  // phase's prefetch and input poll
 #pragma unroll
   for (int j = 0; j < kNBUF; ++j) compute<WFMT, KIND, VPL>(P, b + j, W.b[j], h, red, T);
   __syncthreads();
-  if (a.detail && T.tid == 0) a.detail[((size_t)kb * gridDim.x + blockIdx.x) * 2 + 1] = wall_clock64();
-  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, T);
+  stamp_detail(a, slot, 1);
+  epilogue<WFMT, KIND>(a, P, layer, pos, token, red, sm, xpre, T, ver_of(ep0, k), ep0);
+  if (KIND != K_LM) {
+    stamp(a.bar_arrive, k);
+    if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
+  }
 }
 
 // Issue the first kNBUF batches of a matrix phase into the buffers.
@@ -614,13 +764,6 @@ AIO_DEV void prefetch(const MegaArgs& a, int layer, Bufs& W) {
 }
 
 // ---------------------------------------------------------------- attention
-
-// 16-byte load through a global-address-space pointer (the KV base comes
-// from a table in memory, so the compiler cannot infer the address space).
-AIO_DEV uint4 ldg16(const uint16_t* p) {
-  const u32x4 v = *(gl_u32x4*)p;
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
 
 // One DPP lane move of a float (a VALU operation: no LDS round trip).
 template <int CTRL>
@@ -644,12 +787,18 @@ AIO_DEV float group_sum_dpp(float v) {
 }
 
 // Online-softmax update of one group with one key row (already loaded).  A
-// key past the group's range (valid false) leaves the state unchanged; the
-// masking is done with selects so that the loop has no divergent branches.
+// key past the group's range (valid false) leaves the state unchanged: its
+// row (a dummy read, possibly of a position not yet written) is replaced by
+// zeros, so no stray Inf or NaN can enter, and the masking is done with
+// selects so that the loop has no divergent branches.
 template <int HD, int G>
-AIO_DEV void attend_key(const uint4 kk, const uint4 vv, bool valid, const float (&q)[G][8],
+AIO_DEV void attend_key(uint4 kk, uint4 vv, bool valid, const float (&q)[G][8],
                         float (&o)[G][8], float (&m)[G], float (&l)[G]) {
   constexpr int LPK = HD / 8;
+  // component-wise: a select of whole vectors is built as an indexed copy
+  // in scratch memory
+  kk = make_uint4(valid ? kk.x : 0u, valid ? kk.y : 0u, valid ? kk.z : 0u, valid ? kk.w : 0u);
+  vv = make_uint4(valid ? vv.x : 0u, valid ? vv.y : 0u, valid ? vv.z : 0u, valid ? vv.w : 0u);
   const float vf[8] = {bf16_lo(vv.x), bf16_hi(vv.x), bf16_lo(vv.y), bf16_hi(vv.y),
                        bf16_lo(vv.z), bf16_hi(vv.z), bf16_lo(vv.w), bf16_hi(vv.w)};
 #pragma unroll
@@ -672,17 +821,139 @@ struct KV4 {
   uint4 k[4], v[4];
 };
 
-// Workgroup unit = (kv head g, split s) of the keys [0, pos].  HD/8 lanes
-// hold one key row; each group of lanes runs an online softmax over its keys,
-// the groups combine in LDS, and the split's (max, sum, unnormalised output)
-// goes out as a partial.  The last split of a kv head to finish merges the S
-// partials into o.  Keys stream through two sets of registers in turn (four
-// keys each): one set is in flight while the other is consumed, with no
-// copies between them, so the loads of the next keys are never waited for
-// early.  The first keys are requested before q, the group combine is split
-// four ways, and the merge loads all partials before reducing them.
+// Work unit = (kv head g, split s).  The cached keys [0, pos) are split into
+// S even chunks; HD/8 lanes hold one key row, and group gi of a split takes
+// keys j + t * NGR (t < nk).  nkw is nk of the first group of the wave, the
+// largest in the wave, so the key loop has a wave-uniform trip count.
+struct AUnit {
+  const uint16_t* kb;  // K rows of kv head g, at this lane's 8 dims
+  const uint16_t* vb;
+  int g, s, j, nk, nkw, jd;  // jd: a row read by masked slots
+};
+
+template <int HD>
+AIO_DEV AUnit attn_unit(const MegaArgs& a, int layer, int unit, int pos, const Thr& T) {
+  constexpr int LPK = HD / 8, NGR = kT / LPK, GPW = AIO_WAVE / LPK;
+  const int S = a.S;
+  AUnit u;
+  u.g = unit / S;
+  u.s = unit % S;
+  const int chunk = (pos + S - 1) / S;
+  const int j0 = min(pos, u.s * chunk), j1 = min(pos, j0 + chunk);
+  const int n = j1 - j0;
+  const int gi = T.tid / LPK, li = T.tid % LPK, gw = T.wave * GPW;
+  u.j = j0 + gi;
+  u.nk = n > gi ? (n - gi + NGR - 1) / NGR : 0;
+  u.nkw = __builtin_amdgcn_readfirstlane(n > gw ? (n - gw + NGR - 1) / NGR : 0);
+  u.jd = j1 > j0 ? j1 - 1 : 0;
+  const CMegaLayer* L = layer_at(a, layer);
+  u.kb = L->kc + (size_t)u.g * a.max_ctx * HD + li * 8;
+  u.vb = L->vc + (size_t)u.g * a.max_ctx * HD + li * 8;
+  return u;
+}
+
+// Keys t0 .. t0+3 of this lane's group (unconditional loads; a slot past the
+// group's keys reads row jd and is masked when consumed).
+template <int HD>
+AIO_DEV void load4(const AUnit& u, KV4& d, int t0) {
+  constexpr int NGR = kT / (HD / 8);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = t0 + i;
+    const size_t off = (size_t)(t < u.nk ? u.j + t * NGR : u.jd) * HD;
+    d.k[i] = ldg16(u.kb + off);
+    d.v[i] = ldg16(u.vb + off);
+  }
+}
+
+// The first eight keys of this workgroup's first unit, requested as soon as
+// its QKV rows are out: the cached keys do not depend on this step.
+template <int HD>
+AIO_DEV void attn_prefetch(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y) {
+  const int units = a.Hkv * a.S;
+  const int unit = (int)blockIdx.x < units ? (int)blockIdx.x : units - 1;
+  const AUnit u = attn_unit<HD>(a, layer, unit, pos, thr());
+  load4<HD>(u, X, 0);
+  load4<HD>(u, Y, 4);
+}
+
+// Merge the S split partials of kv head g (its G query heads) into o.
+// Thread (r, c) folds splits r, r + R, ... of output c with a running
+// log-sum-exp; the R partial folds then meet in LDS.  All loads of a thread
+// are issued before its first wait.
 template <int HD, int G>
-AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem& sm) {
+AIO_DEV void attn_merge(const MegaArgs& a, int g, float* lds, unsigned ver) {
+  constexpr int NOUT = G * HD, R = kT / NOUT, MS = 16;
+  const Thr T = thr();
+  const int tid = T.tid, c = tid % NOUT, r = tid / NOUT, gg = c / HD, dim = c % HD;
+  const int S = a.S;
+  const unsigned* base = a.part + (size_t)g * G * S * (HD + 2);
+  float Mt = -INFINITY, Lt = 0.f, Ot = 0.f;
+  for (int s0 = r; s0 < S; s0 += MS * R) {
+    int off[3 * MS];
+    bool need[3 * MS];
+    unsigned v[3 * MS];
+#pragma unroll
+    for (int i = 0; i < MS; ++i) {
+      const int s = s0 + i * R;
+      const bool ok = s < S;
+      const int so = (gg * S + (ok ? s : 0)) * (HD + 2);
+      off[3 * i] = so + dim;
+      off[3 * i + 1] = so + HD;
+      off[3 * i + 2] = so + HD + 1;
+      need[3 * i] = need[3 * i + 1] = need[3 * i + 2] = ok;
+    }
+#pragma unroll
+    for (int i = 0; i < 3 * MS; ++i) v[i] = ld_dev(base + off[i]);
+    await4(a, base, off, need, v, ver);
+#pragma unroll
+    for (int i = 0; i < MS; ++i) {
+      const float ms = untagf(v[3 * i + 1]);
+      if (need[3 * i] && ms != -INFINITY) {
+        const float mn = fmaxf(Mt, ms);
+        const float c0 = exp2f(Mt - mn), c1 = exp2f(ms - mn);
+        Ot = Ot * c0 + c1 * untagf(v[3 * i]);
+        Lt = Lt * c0 + c1 * untagf(v[3 * i + 2]);
+        Mt = mn;
+      }
+    }
+  }
+  float* sm_M = lds;              // [R][G]
+  float* sm_L = lds + R * G;      // [R][G]
+  float* sm_O = lds + 2 * R * G;  // [R][NOUT]
+  if (dim == 0) {
+    sm_M[r * G + gg] = Mt;
+    sm_L[r * G + gg] = Lt;
+  }
+  sm_O[r * NOUT + c] = Ot;
+  __syncthreads();
+  if (tid < NOUT) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < R; ++k) M = fmaxf(M, sm_M[k * G + gg]);
+    float Os = 0.f, Ls = 0.f;
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      const float mk = sm_M[k * G + gg];
+      const float w = mk == -INFINITY ? 0.f : exp2f(mk - M);
+      Os = fmaf(w, sm_O[k * NOUT + c], Os);
+      Ls = fmaf(w, sm_L[k * G + gg], Ls);
+    }
+    st_tag(a.o + (size_t)(g * G + gg) * HD + dim, Os / Ls, ver);
+  }
+  __syncthreads();
+}
+
+// Attention phase k.  Per unit: poll q of the kv head's G query heads
+// (version of phase k - 1), run the online softmax over the split's keys
+// (the first eight per group already in X and Y), add the new key in the
+// last split, combine the NGR groups in LDS and store the split's (output,
+// max, sum).  Keys stream through the two register sets in turn, one in
+// flight while the other is consumed, with no copies between them.  Then
+// the workgroup merges the heads whose last split it ran.
+template <int HD, int G>
+AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, float* lds,
+                        Smem& sm, unsigned ep0, unsigned k) {
   constexpr int LPK = HD / 8, NGR = kT / LPK;
   constexpr int NOUT = G * HD;            // outputs of a unit
   constexpr int R = kT / NOUT > 0 ? kT / NOUT : 1;  // threads per output
@@ -690,45 +961,54 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem&
   float* sm_m = lds;                      // [NGR][G]
   float* sm_l = lds + NGR * G;            // [NGR][G]
   float* sm_o = lds + 2 * NGR * G;        // [NGR][G][HD]
-  float* sm_r = sm_o + NGR * G * HD;      // [R][NOUT] partial sums, then merge scratch
-  const int tid = thr().tid, gi = tid / LPK, li = tid % LPK;
-  const CMegaLayer* L = layer_at(a, layer);
+  float* sm_r = sm_o + NGR * G * HD;      // [R][NOUT] partial sums, then [R][G]
+  const Thr T = thr();
+  const int tid = T.tid, gi = tid / LPK, li = tid % LPK;
+  const int wv = __builtin_amdgcn_readfirstlane(T.wave);
   const int S = a.S, units = a.Hkv * S;
-  const int n_keys = pos + 1;
-  const int chunk = (n_keys + S - 1) / S;
+  const unsigned vq = ver_of(ep0, k - 1), vo = ver_of(ep0, k);
   for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
-    const int g = unit / S, s = unit % S;
-    const int j0 = s * chunk, j1 = min(n_keys, j0 + chunk);
-    // keys of this group: j = j0 + gi + t * NGR for t < nk.  Loads are
-    // unconditional: key t >= nk reads the last valid key of the split (a
-    // cache hit) and is masked when consumed.
-    const int nk = j1 - j0 > gi ? (j1 - j0 - gi + NGR - 1) / NGR : 0;
-    const int jlast = j1 > j0 ? j1 - 1 : (n_keys - 1);  // a key row of this kv head
-    const uint16_t* kb = L->kc + (size_t)g * a.max_ctx * HD + li * 8;
-    const uint16_t* vb = L->vc + (size_t)g * a.max_ctx * HD + li * 8;
-    auto load4 = [&](KV4& d, int t0) {
+    const AUnit u = attn_unit<HD>(a, layer, unit, pos, T);
+    if (unit != (int)blockIdx.x) {
+      load4<HD>(u, X, 0);
+      load4<HD>(u, Y, 4);
+    }
+    // q at this lane's 8 dims; in wave 0 of the last split also the new K/V row
+    const unsigned* qb = a.q + (size_t)u.g * G * HD;
+    int qoff[2 * G];
+    bool qneed[2 * G];
+    u32x4 qw[2 * G];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = t0 + i;
-        const size_t off = (size_t)(t < nk ? j0 + gi + t * NGR : jlast) * HD;
-        d.k[i] = ldg16(kb + off);
-        d.v[i] = ldg16(vb + off);
-      }
-    };
-    KV4 X, Y;
-    load4(X, 0);
+    for (int i = 0; i < 2 * G; ++i) {
+      qoff[i] = (i >> 1) * HD + li * 8 + 4 * (i & 1);
+      qneed[i] = true;
+      qw[i] = ld16_dev(qb, qoff[i]);
+    }
+    const bool nw = u.s == S - 1 && wv == 0;
+    const unsigned* nb = a.kvn + (size_t)u.g * HD;  // K row; the V row is Hkv * HD further
+    int noff[4];
+    bool nneed[4];
+    u32x4 nwd[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      noff[i] = (i >> 1) * a.Hkv * HD + li * 8 + 4 * (i & 1);
+      nneed[i] = gi == 0;
+    }
+    if (nw) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) nwd[i] = ld16_dev(nb, noff[i]);
+    }
+    await16(a, qb, qoff, qneed, qw, vq);
+    if (unit == (int)blockIdx.x) stamp(a.bar_leave, k - 1);
+    __syncthreads();  // every wave is past the previous phase's use of the LDS
     float q[G][8], o[G][8], m[G], l[G];
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) {
-      const float* qp = a.q + (size_t)(g * G + gg) * HD + li * 8;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) q[gg][i] = ldf_dev(qp + i);
-    }
-#pragma unroll
-    for (int gg = 0; gg < G; ++gg) {
+      const u32x4 q0 = qw[2 * gg], q1 = qw[2 * gg + 1];
+      const unsigned qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        q[gg][i] *= a.scale_log2;
+        q[gg][i] = untagf(qq[i]) * a.scale_log2;
         o[gg][i] = 0.f;
       }
       m[gg] = -INFINITY;
@@ -736,17 +1016,32 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem&
     }
     // The scheduling barriers keep each set's loads where they are written:
     // hoisted together, both sets would be waited for at the top of the loop.
-    for (int t = 0; t < nk; t += 8) {
-      load4(Y, t + 4);
+    int t = 0;
+    for (; t + 8 < u.nkw; t += 8) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) attend_key<HD, G>(X.k[i], X.v[i], t + i < u.nk, q, o, m, l);
+      __builtin_amdgcn_sched_barrier(0);
+      load4<HD>(u, X, t + 8);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) attend_key<HD, G>(X.k[i], X.v[i], t + i < nk, q, o, m, l);
+      for (int i = 0; i < 4; ++i) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < u.nk, q, o, m, l);
       __builtin_amdgcn_sched_barrier(0);
-      load4(X, t + 8);
+      load4<HD>(u, Y, t + 12);
       __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < nk, q, o, m, l);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < 4; ++i) attend_key<HD, G>(X.k[i], X.v[i], t + i < u.nk, q, o, m, l);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < u.nk, q, o, m, l);
+    if (nw) {
+      // the new key (position pos), taken by group 0 of the last split
+      await16(a, nb, noff, nneed, nwd, vq);
+      const u32x4 k0 = nwd[0], k1 = nwd[1], v0 = nwd[2], v1 = nwd[3];
+      const uint4 kk = make_uint4((k0.x >> 16) | (k0.y & 0xffff0000u), (k0.z >> 16) | (k0.w & 0xffff0000u),
+                                  (k1.x >> 16) | (k1.y & 0xffff0000u), (k1.z >> 16) | (k1.w & 0xffff0000u));
+      const uint4 vv = make_uint4((v0.x >> 16) | (v0.y & 0xffff0000u), (v0.z >> 16) | (v0.w & 0xffff0000u),
+                                  (v1.x >> 16) | (v1.y & 0xffff0000u), (v1.z >> 16) | (v1.w & 0xffff0000u));
+      attend_key<HD, G>(kk, vv, gi == 0, q, o, m, l);
     }
     // combine the NGR groups: R threads per output, NGR / R groups each
 #pragma unroll
@@ -759,19 +1054,18 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem&
       for (int i = 0; i < 8; ++i) sm_o[(gi * G + gg) * HD + li * 8 + i] = o[gg][i];
     }
     __syncthreads();
-    float* part = a.part + (size_t)g * G * S * (HD + 2);
     {
       const int c = tid % NOUT, r = tid / NOUT;  // output c, part r
       const int gg = c / HD, dim = c % HD;
       float M = -INFINITY;
-      for (int k = 0; k < NGR; ++k) M = fmaxf(M, sm_m[k * G + gg]);
+      for (int kk = 0; kk < NGR; ++kk) M = fmaxf(M, sm_m[kk * G + gg]);
       float Ls = 0.f, Os = 0.f;
       if (r < R && M != -INFINITY) {
-        for (int k = r * (NGR / R); k < (r + 1) * (NGR / R); ++k) {
-          const float mk = sm_m[k * G + gg];
+        for (int kk = r * (NGR / R); kk < (r + 1) * (NGR / R); ++kk) {
+          const float mk = sm_m[kk * G + gg];
           const float w = mk == -INFINITY ? 0.f : exp2f(mk - M);
-          Ls = fmaf(w, sm_l[k * G + gg], Ls);
-          Os = fmaf(w, sm_o[(k * G + gg) * HD + dim], Os);
+          Ls = fmaf(w, sm_l[kk * G + gg], Ls);
+          Os = fmaf(w, sm_o[(kk * G + gg) * HD + dim], Os);
         }
       }
       __syncthreads();
@@ -783,77 +1077,26 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, float* lds, Smem&
       if (tid < NOUT) {
         float Ot = 0.f, Lt = 0.f;
 #pragma unroll
-        for (int k = 0; k < R; ++k) {
-          Ot += sm_r[k * NOUT + c];
-          Lt += sm_r[R * NOUT + k * G + gg];
+        for (int kk = 0; kk < R; ++kk) {
+          Ot += sm_r[kk * NOUT + c];
+          Lt += sm_r[R * NOUT + kk * G + gg];
         }
-        float* slot = part + ((size_t)gg * S + s) * (HD + 2);
-        stf_dev(slot + dim, Ot);
+        unsigned* slot = a.part + ((size_t)(u.g * G + gg) * S + u.s) * (HD + 2);
+        st_tag(slot + dim, Ot, vo);
         if (dim == 0) {
-          stf_dev(slot + HD, M);
-          stf_dev(slot + HD + 1, Lt);
+          st_tag(slot + HD, M, vo);
+          st_tag(slot + HD + 1, Lt, vo);
         }
       }
     }
-    wg_publish();
-    if (tid == 0) sm.flag = add_dev(a.sync + kSyncAttn + g, 1u) == (unsigned)(S - 1);
-    __syncthreads();
-    if (sm.flag) {
-      // last split of kv head g: merge the S partials of its G query heads.
-      // 1) all (max, sum) pairs at once
-      float* mm = sm_r;             // [G][S]
-      float* ww = sm_r + G * S;     // [G][S] weights, then [G] totals
-      for (int e = tid; e < G * S; e += kT) {
-        const int gg = e / S, k = e % S;
-        const float* sl = part + ((size_t)gg * S + k) * (HD + 2);
-        mm[e] = ldf_dev(sl + HD);
-        ww[e] = ldf_dev(sl + HD + 1);
-      }
-      __syncthreads();
-      if (tid < G) {
-        float M = -INFINITY;
-        for (int k = 0; k < S; ++k) M = fmaxf(M, mm[tid * S + k]);
-        float Lt = 0.f;
-        for (int k = 0; k < S; ++k) {
-          const float w = mm[tid * S + k] == -INFINITY ? 0.f : exp2f(mm[tid * S + k] - M);
-          Lt = fmaf(w, ww[tid * S + k], Lt);
-          mm[tid * S + k] = w;  // reuse as the weight of split k
-        }
-        ww[G * S + tid] = Lt;
-      }
-      __syncthreads();
-      // 2) R threads per output, each over every R-th split, loads first
-      const int c = tid % NOUT, r = tid / NOUT;
-      const int gg = c / HD, dim = c % HD;
-      float acc = 0.f;
-      if (r < R) {
-        const float* base = part + (size_t)gg * S * (HD + 2) + dim;
-        int k = r;
-        for (; k + 3 * R < S; k += 4 * R) {
-          const float x0 = ldf_dev(base + (size_t)k * (HD + 2));
-          const float x1 = ldf_dev(base + (size_t)(k + R) * (HD + 2));
-          const float x2 = ldf_dev(base + (size_t)(k + 2 * R) * (HD + 2));
-          const float x3 = ldf_dev(base + (size_t)(k + 3 * R) * (HD + 2));
-          acc = fmaf(mm[gg * S + k], x0, acc);
-          acc = fmaf(mm[gg * S + k + R], x1, acc);
-          acc = fmaf(mm[gg * S + k + 2 * R], x2, acc);
-          acc = fmaf(mm[gg * S + k + 3 * R], x3, acc);
-        }
-        for (; k < S; k += R) acc = fmaf(mm[gg * S + k], ldf_dev(base + (size_t)k * (HD + 2)), acc);
-      }
-      float* red = sm_o;  // [R][NOUT]; the group outputs are no longer needed
-      if (r < R) red[r * NOUT + c] = acc;
-      __syncthreads();
-      if (tid < NOUT) {
-        float ot = 0.f;
-#pragma unroll
-        for (int k = 0; k < R; ++k) ot += red[k * NOUT + c];
-        stf_dev(a.o + (size_t)(g * G + gg) * HD + dim, ot / ww[G * S + gg]);
-      }
-      if (tid == 0) st_dev(a.sync + kSyncAttn + g, 0u);
-    }
-    __syncthreads();
+    __syncthreads();  // the LDS is reused by the next unit or the merge
   }
+  stamp_detail(a, k, 0);
+  for (int g = 0; g < a.Hkv; ++g)
+    if ((g * S + S - 1) % (int)gridDim.x == (int)blockIdx.x) attn_merge<HD, G>(a, g, lds, vo);
+  stamp_detail(a, k, 1);
+  stamp(a.bar_arrive, k);
+  if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
 }
 
 template <int WFMT, int HD, int G, int VQ, int VD>
@@ -861,51 +1104,35 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   extern __shared__ float lds[];
   __shared__ Smem sm;
   const int pos = a.st->pos, token = a.st->token[0];
-  // every thread reads the epoch base before the first barrier; workgroup 0
-  // advances it for the next launch once that barrier has passed
+  // the epoch base of this step; the last workgroup of the argmax advances it
   const unsigned ep0 = ld_dev(a.sync + kSyncEpoch);
-  unsigned k = 0;
   Bufs W;
+  KV4 X, Y;
   prefetch<WFMT, HD, K_QKV, VQ>(a, 0, W);
-  auto none = [] {};
   for (int l = 0; l < a.L; ++l) {
-    {
-      const GPhase P = make_phase<WFMT, K_QKV>(a, l);
-      gemv_phase<WFMT, HD, K_QKV, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
-    }
-    grid_sync(a, ep0, ++k, none);
-    if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0)
-      st_dev(a.sync + kSyncEpoch, ep0 + 5u * (unsigned)a.L);
-    attn_phase<HD, G>(a, l, pos, lds, sm);
-    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_O, VQ>(a, l, W); });
-    {
-      const GPhase P = make_phase<WFMT, K_O>(a, l);
-      gemv_phase<WFMT, HD, K_O, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
-    }
-    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_GU, VQ>(a, l, W); });
-    {
-      const GPhase P = make_phase<WFMT, K_GU>(a, l);
-      gemv_phase<WFMT, HD, K_GU, VQ>(a, P, l, pos, token, W, lds, sm, k + 1);
-    }
-    grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_DOWN, VD>(a, l, W); });
-    {
-      const GPhase P = make_phase<WFMT, K_DOWN>(a, l);
-      gemv_phase<WFMT, HD, K_DOWN, VD>(a, P, l, pos, token, W, lds, sm, k + 1);
-    }
+    const unsigned k = 5u * (unsigned)l;
+    gemv_phase<WFMT, HD, K_QKV, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 1);
+    attn_prefetch<HD>(a, l, pos, X, Y);
+    attn_phase<HD, G>(a, l, pos, X, Y, lds, sm, ep0, k + 2);
+    prefetch<WFMT, HD, K_O, VQ>(a, l, W);
+    gemv_phase<WFMT, HD, K_O, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 3);
+    prefetch<WFMT, HD, K_GU, VQ>(a, l, W);
+    gemv_phase<WFMT, HD, K_GU, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 4);
+    prefetch<WFMT, HD, K_DOWN, VD>(a, l, W);
+    gemv_phase<WFMT, HD, K_DOWN, VD>(a, l, pos, token, W, lds, sm, ep0, k + 5);
     if (l + 1 < a.L)
-      grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_QKV, VQ>(a, l + 1, W); });
+      prefetch<WFMT, HD, K_QKV, VQ>(a, l + 1, W);
     else
-      grid_sync(a, ep0, ++k, [&] { prefetch<WFMT, HD, K_LM, VQ>(a, l + 1, W); });
+      prefetch<WFMT, HD, K_LM, VQ>(a, l + 1, W);
   }
-  const GPhase P = make_phase<WFMT, K_LM>(a, a.L);
-  gemv_phase<WFMT, HD, K_LM, VQ>(a, P, a.L, pos, token, W, lds, sm, 0u);
+  gemv_phase<WFMT, HD, K_LM, VQ>(a, a.L, pos, token, W, lds, sm, ep0, 5u * (unsigned)a.L + 1);
 }
 
 // The grid is one workgroup per CU and a CU holds at most one (registers
 // and LDS), so all workgroups are resident together.  The cooperative
 // launch states that requirement to the runtime, which refuses the launch
 // if it cannot be met; a plain launch of the same grid relies on the GPU
-// running nothing else (every barrier wait is bounded either way).
+// running nothing else (every wait is bounded either way).
 template <int WFMT, int HD, int G, int VQ, int VD>
 hipError_t launch_t(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, bool coop) {
   void* args[] = {(void*)&a};
@@ -966,10 +1193,9 @@ size_t aio_step_kernel_lds(const aio_config& c, int blocks) {
   const int ngr = kT / (c.head_dim / 8);
   const int nout = G * c.head_dim;
   const int r = kT / nout > 0 ? kT / nout : 1;
-  const int S = AIO_STEP_MAX_BLOCKS / c.n_kv_heads > 0 ? AIO_STEP_MAX_BLOCKS / c.n_kv_heads : 1;
-  // group state + [R][NOUT] partials (+ R * G sums) or the merge's 2 G S + G
-  const size_t scratch = std::max((size_t)r * nout + (size_t)r * G, (size_t)2 * G * S + G);
-  const size_t attn = ((size_t)ngr * G * (c.head_dim + 2) + scratch) * 4;
+  // group state + [R][NOUT] partials + R * G sums; the merge needs
+  // 2 R G + R NOUT, which fits in the same space
+  const size_t attn = ((size_t)ngr * G * (c.head_dim + 2) + (size_t)r * nout + (size_t)r * G) * 4;
   auto red = [&](int units, int rpu) { return (size_t)((units + blocks - 1) / blocks) * rpu * kW * 4; };
   size_t gemv = red((c.n_heads + 2 * c.n_kv_heads) * c.head_dim / 4, 4);
   gemv = std::max(gemv, red(c.d_model, 1));
@@ -990,11 +1216,13 @@ hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* to
   a.s_lm = (const uint16_t*)m.s_lm_head;
   a.rope = m.rope;
   a.st = m.state();
-  a.x = m.at<float>(m.lay.x);
-  a.q = m.at<float>(m.lay.q);
-  a.o = m.at<float>(m.lay.o);
-  a.m = m.at<float>(m.lay.m);
-  a.part = m.at<float>(m.lay.mega_part);
+  a.xa = m.at<unsigned>(m.lay.mega_xa);
+  a.xb = m.at<unsigned>(m.lay.mega_xb);
+  a.q = m.at<unsigned>(m.lay.mega_q);
+  a.kvn = m.at<unsigned>(m.lay.mega_kvn);
+  a.o = m.at<unsigned>(m.lay.mega_o);
+  a.m = m.at<unsigned>(m.lay.mega_m);
+  a.part = m.at<unsigned>(m.lay.mega_part);
   a.sync = m.at<unsigned>(m.lay.sync);
   a.logits = logits;
   a.tokens_out = tokens_out;
