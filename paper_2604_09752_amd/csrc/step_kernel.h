@@ -57,6 +57,7 @@ struct MegaArgs {
   unsigned long long* bar_leave;   // optional: [5 L + 1][blocks] time the inputs of phase k + 1 were in
   unsigned long long* detail;      // optional: [5 L + 1][blocks][2] loop start and end of phase k
   int L, d, H, Hkv, hd, F, V, max_ctx, S;
+  int red_words;   // floats of one LDS buffer of matrix-phase partials
   float eps, scale_log2;
 };
 

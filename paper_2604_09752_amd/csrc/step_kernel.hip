@@ -169,38 +169,50 @@ struct Unroll<N, N> {
 };
 
 // Wait until the loaded 16-byte words this thread needs carry version `ver`,
-// reloading only the stale ones.
+// reloading only the stale ones.  The first check sits outside the retry
+// loop: there the compiler knows which loads were issued after the words
+// (the next weight batch) and waits only for the words themselves.
+template <int N>
+AIO_DEV bool stale16(const bool (&need)[N], const u32x4 (&v)[N], unsigned ver) {
+  bool stale = false;
+  Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+    stale |= need[i] && !tags_ok(v[i], ver);
+  });
+  return stale;
+}
 template <int N>
 AIO_DEV void await16(const MegaArgs& a, const unsigned* base, const int (&off)[N],
                      const bool (&need)[N], u32x4 (&v)[N], unsigned ver) {
+  if (!stale16(need, v, ver)) return;
   unsigned spins = 0;
-  for (;;) {
-    bool stale = false;
-    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
-      stale |= need[i] && !tags_ok(v[i], ver);
-    });
-    if (!stale || !spin_on(a, spins)) break;
+  do {
+    if (!spin_on(a, spins)) break;
     Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
       if (need[i] && !tags_ok(v[i], ver)) v[i] = ld16_dev(base, off[i]);
     });
-  }
+  } while (stale16(need, v, ver));
 }
 
 // The same for single words.
 template <int N>
+AIO_DEV bool stale4(const bool (&need)[N], const unsigned (&v)[N], unsigned ver) {
+  bool stale = false;
+  Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
+    stale |= need[i] && (v[i] & 7u) != ver;
+  });
+  return stale;
+}
+template <int N>
 AIO_DEV void await4(const MegaArgs& a, const unsigned* base, const int (&off)[N],
                     const bool (&need)[N], unsigned (&v)[N], unsigned ver) {
+  if (!stale4(need, v, ver)) return;
   unsigned spins = 0;
-  for (;;) {
-    bool stale = false;
-    Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
-      stale |= need[i] && (v[i] & 7u) != ver;
-    });
-    if (!stale || !spin_on(a, spins)) break;
+  do {
+    if (!spin_on(a, spins)) break;
     Unroll<0, N>::run([&](int i) __attribute__((always_inline)) {
       if (need[i] && (v[i] & 7u) != ver) v[i] = ld_dev(base + off[i]);
     });
-  }
+  } while (stale4(need, v, ver));
 }
 
 // Optional timing records (profiling aids; null in normal runs).
@@ -397,7 +409,7 @@ AIO_DEV float reduce_rows(float (&v)[kNLD], int lane) {
 
 // Multiply-accumulate one batch and leave each wave's row partials in LDS
 // red[(local unit * RPU + r) * kW + wave].  Slots are not masked here: a
-// lane past the end of its K-slice holds h = 0 (load_input) and reads a
+// lane past the end of its K-slice holds h = 0 (input_finish) and reads a
 // vector of the same row, so it adds an exact zero for finite weights; a
 // unit past the workgroup's range is dropped at the LDS write.
 template <int WFMT, int KIND, int VPL>
@@ -435,17 +447,29 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
 
 // This lane's slice of the phase input, normalised when the phase starts
 // with an RMSNorm.  The slice of wave w, vector v is elements
-// [(w * nvw + v * 64 + lane) * EPV, +EPV).  The norm gains are requested
-// first (they do not depend on other workgroups), then the input words,
-// which are polled until they carry version `ver`.
+// [(w * nvw + v * 64 + lane) * EPV, +EPV).  Issued in two steps so that the
+// caller can put the phase's second weight batch between the input loads
+// and the wait for them: vector memory returns in order, so a wait queued
+// behind less prefetch sees the input sooner.
 template <int WFMT, int KIND, int VPL>
-AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token, unsigned ver,
-                        float (&h)[VPL][epv<WFMT>()], float* red8, const Thr& T) {
-  constexpr int E = epv<WFMT>(), NQ = E / 4, NG = E / 8;
+struct Input {
+  static constexpr int E = epv<WFMT>(), NQ = E / 4, NG = E / 8, N = VPL * NQ;
+  uint4 gw[VPL][NG];  // norm gains (bf16)
+  int off[N];         // word offsets of the input vectors
+  bool need[N];
+  u32x4 w[N];
+};
+
+// Step 1: request the norm gains (they do not depend on other workgroups)
+// and the input words.
+template <int WFMT, int KIND, int VPL>
+AIO_DEV void input_issue(const MegaArgs& a, const GPhase& P, int layer, Input<WFMT, KIND, VPL>& I,
+                         const Thr& T) {
+  using In = Input<WFMT, KIND, VPL>;
+  constexpr int E = In::E, NQ = In::NQ, NG = In::NG;
   constexpr bool NORM = KIND == K_QKV || KIND == K_GU || KIND == K_LM;
   const int lane = T.lane, wave = T.wave;
   const bool any = P.u1 > P.u0;  // a workgroup with no rows reads nothing
-  uint4 gw[VPL][NG];
   if constexpr (NORM) {
     const CMegaLayer* L = layer_at(a, layer < a.L ? layer : 0);
     const uint16_t* g = KIND == K_QKV ? L->attn_norm : (KIND == K_GU ? L->ffn_norm : a.final_norm);
@@ -454,9 +478,39 @@ AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token
       const int vi = v * AIO_WAVE + lane;
       const int e0 = (wave * P.nvw + (vi < P.nvw ? vi : 0)) * E;
 #pragma unroll
-      for (int j = 0; j < NG; ++j) gw[v][j] = ldg16(g + e0 + 8 * j);
+      for (int j = 0; j < NG; ++j) I.gw[v][j] = ldg16(g + e0 + 8 * j);
     }
   }
+  if (KIND == K_QKV && layer == 0) return;  // the embedding row: read in step 2
+  const unsigned* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : (KIND == K_GU ? a.xa : a.xb));
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    const int vi = v * AIO_WAVE + lane;
+    const bool ok = vi < P.nvw;
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+      I.off[v * NQ + j] = (wave * P.nvw + (ok ? vi : 0)) * E + 4 * j;
+      I.need[v * NQ + j] = any && ok;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < In::N; ++i) I.w[i] = ld16_dev(src, I.off[i]);
+}
+
+// Step 2: wait until the input words carry version `ver` and unpack them.
+// Nothing here waits for the other waves: each wave starts its loop as soon
+// as its own slice is in.  The RMSNorm is applied in two parts: the gains
+// here (h = g * x) and the scalar 1 / rms(x) in the epilogue, after the
+// products (it is the same for every row); this wave's share of sum(x^2)
+// goes to ss8[wave].
+template <int WFMT, int KIND, int VPL>
+AIO_DEV void input_finish(const MegaArgs& a, const GPhase& P, int layer, int token, unsigned ver,
+                          Input<WFMT, KIND, VPL>& I, float (&h)[VPL][epv<WFMT>()], float* ss8,
+                          const Thr& T) {
+  using In = Input<WFMT, KIND, VPL>;
+  constexpr int E = In::E, NQ = In::NQ, NG = In::NG;
+  constexpr bool NORM = KIND == K_QKV || KIND == K_GU || KIND == K_LM;
+  const int lane = T.lane, wave = T.wave;
   if (KIND == K_QKV && layer == 0) {
     const uint16_t* er = a.embed + (size_t)token * a.d;
 #pragma unroll
@@ -477,28 +531,13 @@ AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token
     }
   } else {
     const unsigned* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : (KIND == K_GU ? a.xa : a.xb));
-    int off[VPL * NQ];
-    bool need[VPL * NQ];
-    u32x4 w[VPL * NQ];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      const int vi = v * AIO_WAVE + lane;
-      const bool ok = vi < P.nvw;
-#pragma unroll
-      for (int j = 0; j < NQ; ++j) {
-        off[v * NQ + j] = (wave * P.nvw + (ok ? vi : 0)) * E + 4 * j;
-        need[v * NQ + j] = any && ok;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VPL * NQ; ++i) w[i] = ld16_dev(src, off[i]);
-    await16(a, src, off, need, w, ver);
+    await16(a, src, I.off, I.need, I.w, ver);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
 #pragma unroll
       for (int j = 0; j < NQ; ++j) {
-        const u32x4 x = w[v * NQ + j];
-        const bool ok = need[v * NQ + j];
+        const u32x4 x = I.w[v * NQ + j];
+        const bool ok = I.need[v * NQ + j];
         h[v][4 * j + 0] = ok ? untagf(x.x) : 0.f;
         h[v][4 * j + 1] = ok ? untagf(x.y) : 0.f;
         h[v][4 * j + 2] = ok ? untagf(x.z) : 0.f;
@@ -514,28 +553,19 @@ AIO_DEV void load_input(const MegaArgs& a, const GPhase& P, int layer, int token
       for (int i = 0; i < E; ++i) ss = fmaf(h[v][i], h[v][i], ss);
     }
     ss = wave_sum(ss);
-    if (lane == 0) red8[wave] = ss;
-    __syncthreads();
-    float tot = 0.f;
-#pragma unroll
-    for (int w8 = 0; w8 < kW; ++w8) tot += red8[w8];
-    __syncthreads();  // red8 is reused by the next phase
-    const float inv = rsqrtf(tot / (float)P.K + a.eps);
+    if (lane == 0) ss8[wave] = ss;
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
 #pragma unroll
       for (int j = 0; j < NG; ++j) {
-        const uint32_t g4[4] = {gw[v][j].x, gw[v][j].y, gw[v][j].z, gw[v][j].w};
+        const uint32_t g4[4] = {I.gw[v][j].x, I.gw[v][j].y, I.gw[v][j].z, I.gw[v][j].w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          h[v][8 * j + 2 * i] = h[v][8 * j + 2 * i] * inv * bf16_lo(g4[i]);
-          h[v][8 * j + 2 * i + 1] = h[v][8 * j + 2 * i + 1] * inv * bf16_hi(g4[i]);
+          h[v][8 * j + 2 * i] *= bf16_lo(g4[i]);
+          h[v][8 * j + 2 * i + 1] *= bf16_hi(g4[i]);
         }
       }
     }
-  } else {
-    // every wave is past the previous phase's reads of the LDS partials
-    __syncthreads();
   }
 }
 
@@ -565,28 +595,26 @@ AIO_DEV void block_argmax(float& bv, int& bi, float* sv, int* si) {
 }
 
 struct Smem {
-  float red8[kW];
+  float ss8[2][kW];  // per-wave sum(x^2) of a normed phase, by phase parity
   float sv[kW];
   int si[kW];
   unsigned flag;
 };
 
-// Residual row u before a phase that adds to it: the embedding row at the
-// first O projection, else this workgroup's own output of two phases back
-// (O reads the DOWN output, DOWN reads the O output; same rows, same
-// thread, so no wait).
+// Residual row u (tagged word) before a phase that adds to it: this
+// workgroup's own output of two phases back (O reads the DOWN output, or at
+// the first layer the embedding row stored at the start of the step; DOWN
+// reads the O output).  Same rows, same thread, so no wait.
 template <int KIND>
-AIO_DEV float resid(const MegaArgs& a, int layer, int token, int u) {
-  if (KIND == K_O && layer == 0) return bf16_to_f32(a.embed[(size_t)token * a.d + u]);
-  return untagf(ld_dev((KIND == K_O ? a.xb : a.xa) + u));
+AIO_DEV unsigned resid(const MegaArgs& a, int u) {
+  return ld_dev((KIND == K_O ? a.xb : a.xa) + u);
 }
 
 // Epilogue of a matrix phase: sum the kW wave partials of each row, then the
 // phase-specific output, stored with version `vo`.
 template <int WFMT, int KIND>
-AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, int token,
-                      const float* red, Smem& sm, float xpre, const Thr& T, unsigned vo,
-                      unsigned ep0) {
+AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, const float* red,
+                      Smem& sm, unsigned xpre, float inv, const Thr& T, unsigned vo, unsigned ep0) {
   constexpr int RPU = rpu_of<KIND>();
   const int nu = P.u1 - P.u0;
   const int tid = T.tid;
@@ -599,7 +627,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, in
       float s = 0.f;
 #pragma unroll
       for (int w = 0; w < kW; ++w) s += red[(t * RPU + r) * kW + w];
-      y[r] = s;
+      y[r] = KIND == K_O || KIND == K_DOWN ? s : s * inv;  // 1 / rms of a normed input
     }
     const int u = P.u0 + t;
     if constexpr (KIND == K_QKV) {
@@ -660,7 +688,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, in
         a.logits[u] = yy;
         if (am_better(yy, u, bv, bi)) { bv = yy; bi = u; }
       } else {
-        const float xo = t == tid ? xpre : resid<KIND>(a, layer, token, u);
+        const float xo = untagf(t == tid ? xpre : resid<KIND>(a, u));
         st_tag((KIND == K_O ? a.xa : a.xb) + u, xo + yy, vo);
       }
     }
@@ -704,32 +732,45 @@ struct Bufs {
   uint4 b[kNBUF][kNLD];
 };
 
-// Matrix phase k.  On entry buffer j holds (in flight) batch j of this
+// Matrix phase k.  On entry buffer 0 holds (in flight) batch 0 of this
 // phase; each buffer is refilled with the phase's batch kNBUF further on as
 // soon as it is consumed.
 template <int WFMT, int HD, int KIND, int VPL>
-AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& W, float* red,
+AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& W, float* lds,
                         Smem& sm, unsigned ep0, unsigned k) {
   constexpr int RPU = rpu_of<KIND>();
+  // LDS partials and norm sums alternate between two buffers by phase
+  // parity: a wave may start this phase while another still reads the
+  // previous phase's partials in its epilogue
+  float* red = lds + (k & 1u) * (unsigned)a.red_words;
+  float* ss8 = sm.ss8[k & 1u];
   constexpr int UB = kNLD / (RPU * VPL);
   const GPhase P = make_phase<WFMT, KIND>(a, layer);
   const int nb = (P.u1 - P.u0 + UB - 1) / UB;
   const unsigned slot = KIND == K_LM ? 0u : k;  // timing slot
   const Thr T = thr();
   // residual rows this workgroup will update, fetched now to hide the trip
-  float xpre = 0.f;
+  // (unconditionally, and kept tagged until the epilogue: a load under a
+  // branch, or an early use, would be waited for here behind batch 0)
+  unsigned xpre = 0u;
   if (KIND == K_O || KIND == K_DOWN) {
-    if (T.tid < P.u1 - P.u0) xpre = resid<KIND>(a, layer, token, P.u0 + T.tid);
+    const int t = T.tid < P.u1 - P.u0 ? T.tid : 0;
+    xpre = resid<KIND>(a, P.u0 + t < a.d ? P.u0 + t : a.d - 1);
   }
+  // batch 0 is in flight (prefetch); then the input words, then the other
+  // batches, so the wait for the input is queued behind one batch only
+  // (the scheduling barriers keep the three groups of loads, and the first
+  // check of the input, in this order)
+  Input<WFMT, KIND, VPL> I;
+  input_issue<WFMT, KIND, VPL>(a, P, layer, I, T);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int j = 1; j < kNBUF; ++j) issue<WFMT, KIND, VPL, HD>(a, P, j, W.b[j], T);
+  __builtin_amdgcn_sched_barrier(0);
   float h[VPL][epv<WFMT>()];
-  load_input<WFMT, KIND, VPL>(a, P, layer, token, ver_of(ep0, k - 1), h, sm.red8, T);
+  input_finish<WFMT, KIND, VPL>(a, P, layer, token, ver_of(ep0, k - 1), I, h, ss8, T);
   stamp(a.bar_leave, k - 1);
   stamp_detail(a, slot, 0);
-  // The input loads above were issued after this phase's first batches,
-  // so waiting for them has waited for everything; say so explicitly
-  // (vmcnt(0)), so that the loop below starts from a state in which only
-  // its own loads are in flight and waits only for the buffer it consumes.
-  __builtin_amdgcn_s_waitcnt(kVmcnt0);
   // Branch-free body: a batch past the end is computed fully masked and its
   // refill is a masked dummy (cache-hit) load, so the compiler sees the same
   // loads in flight behind each buffer on every path.
@@ -747,20 +788,26 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
   for (int j = 0; j < kNBUF; ++j) compute<WFMT, KIND, VPL>(P, b + j, W.b[j], h, red, T);
   __syncthreads();
   stamp_detail(a, slot, 1);
-  epilogue<WFMT, KIND>(a, P, layer, pos, token, red, sm, xpre, T, ver_of(ep0, k), ep0);
+  float inv = 1.f;
+  if (KIND == K_QKV || KIND == K_GU || KIND == K_LM) {
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) tot += ss8[w];
+    inv = rsqrtf(tot / (float)P.K + a.eps);
+  }
+  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, inv, T, ver_of(ep0, k), ep0);
   if (KIND != K_LM) {
     stamp(a.bar_arrive, k);
     if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
   }
 }
 
-// Issue the first kNBUF batches of a matrix phase into the buffers.
+// Issue the first batch of a matrix phase into buffer 0 (the phase itself
+// issues the others once its input words are requested).
 template <int WFMT, int HD, int KIND, int VPL>
 AIO_DEV void prefetch(const MegaArgs& a, int layer, Bufs& W) {
   const GPhase N = make_phase<WFMT, KIND>(a, layer);
-  const Thr T = thr();
-#pragma unroll
-  for (int j = 0; j < kNBUF; ++j) issue<WFMT, KIND, VPL, HD>(a, N, j, W.b[j], T);
+  issue<WFMT, KIND, VPL, HD>(a, N, 0, W.b[0], thr());
 }
 
 // ---------------------------------------------------------------- attention
@@ -866,15 +913,15 @@ AIO_DEV void load4(const AUnit& u, KV4& d, int t0) {
   }
 }
 
-// The first eight keys of this workgroup's first unit, requested as soon as
-// its QKV rows are out: the cached keys do not depend on this step.
+// The first four keys of each group of this workgroup's first unit,
+// requested as soon as its QKV rows are out: the cached keys do not depend
+// on this step.  The next four follow the poll for q.
 template <int HD>
-AIO_DEV void attn_prefetch(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y) {
+AIO_DEV void attn_prefetch(const MegaArgs& a, int layer, int pos, KV4& X) {
   const int units = a.Hkv * a.S;
   const int unit = (int)blockIdx.x < units ? (int)blockIdx.x : units - 1;
   const AUnit u = attn_unit<HD>(a, layer, unit, pos, thr());
   load4<HD>(u, X, 0);
-  load4<HD>(u, Y, 4);
 }
 
 // Merge the S split partials of kv head g (its G query heads) into o.
@@ -969,10 +1016,7 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
   const unsigned vq = ver_of(ep0, k - 1), vo = ver_of(ep0, k);
   for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
     const AUnit u = attn_unit<HD>(a, layer, unit, pos, T);
-    if (unit != (int)blockIdx.x) {
-      load4<HD>(u, X, 0);
-      load4<HD>(u, Y, 4);
-    }
+    if (unit != (int)blockIdx.x) load4<HD>(u, X, 0);
     // q at this lane's 8 dims; in wave 0 of the last split also the new K/V row
     const unsigned* qb = a.q + (size_t)u.g * G * HD;
     int qoff[2 * G];
@@ -998,9 +1042,11 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
 #pragma unroll
       for (int i = 0; i < 4; ++i) nwd[i] = ld16_dev(nb, noff[i]);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    load4<HD>(u, Y, 4);
+    __builtin_amdgcn_sched_barrier(0);
     await16(a, qb, qoff, qneed, qw, vq);
     if (unit == (int)blockIdx.x) stamp(a.bar_leave, k - 1);
-    __syncthreads();  // every wave is past the previous phase's use of the LDS
     float q[G][8], o[G][8], m[G], l[G];
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) {
@@ -1109,11 +1155,19 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   Bufs W;
   KV4 X, Y;
   prefetch<WFMT, HD, K_QKV, VQ>(a, 0, W);
+  {
+    // the residual before layer 0 (the embedding row) of the rows this
+    // workgroup updates in the O projection
+    const GPhase P = make_phase<WFMT, K_O>(a, 0);
+    const int t = thr().tid;
+    if (t < P.u1 - P.u0)
+      st_tag(a.xb + P.u0 + t, bf16_to_f32(a.embed[(size_t)token * a.d + P.u0 + t]), ver_of(ep0, 0));
+  }
   for (int l = 0; l < a.L; ++l) {
     const unsigned k = 5u * (unsigned)l;
     gemv_phase<WFMT, HD, K_QKV, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 1);
-    attn_prefetch<HD>(a, l, pos, X, Y);
-    attn_phase<HD, G>(a, l, pos, X, Y, lds, sm, ep0, k + 2);
+    attn_prefetch<HD>(a, l, pos, X);
+    attn_phase<HD, G>(a, l, pos, X, Y, lds + 2 * a.red_words, sm, ep0, k + 2);
     prefetch<WFMT, HD, K_O, VQ>(a, l, W);
     gemv_phase<WFMT, HD, K_O, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 3);
     prefetch<WFMT, HD, K_GU, VQ>(a, l, W);
@@ -1188,6 +1242,16 @@ bool aio_step_kernel_supports(const aio_config& c) {
   return true;
 }
 
+// Floats of one buffer of matrix-phase partials: [units per workgroup][RPU][kW].
+static int red_words(const aio_config& c, int blocks) {
+  auto red = [&](int units, int rpu) { return ((units + blocks - 1) / blocks) * rpu * kW; };
+  int w = red((c.n_heads + 2 * c.n_kv_heads) * c.head_dim / 4, 4);
+  w = std::max(w, red(c.d_model, 1));
+  w = std::max(w, red(c.ffn_dim, 2));
+  w = std::max(w, red(c.vocab, 1));
+  return (w + 63) & ~63;
+}
+
 size_t aio_step_kernel_lds(const aio_config& c, int blocks) {
   const int G = c.n_heads / c.n_kv_heads;
   const int ngr = kT / (c.head_dim / 8);
@@ -1196,12 +1260,8 @@ size_t aio_step_kernel_lds(const aio_config& c, int blocks) {
   // group state + [R][NOUT] partials + R * G sums; the merge needs
   // 2 R G + R NOUT, which fits in the same space
   const size_t attn = ((size_t)ngr * G * (c.head_dim + 2) + (size_t)r * nout + (size_t)r * G) * 4;
-  auto red = [&](int units, int rpu) { return (size_t)((units + blocks - 1) / blocks) * rpu * kW * 4; };
-  size_t gemv = red((c.n_heads + 2 * c.n_kv_heads) * c.head_dim / 4, 4);
-  gemv = std::max(gemv, red(c.d_model, 1));
-  gemv = std::max(gemv, red(c.ffn_dim, 2));
-  gemv = std::max(gemv, red(c.vocab, 1));
-  return std::max(attn, gemv);
+  // attention area after the two matrix-phase partial buffers
+  return (size_t)2 * red_words(c, blocks) * 4 + attn;
 }
 
 hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* tokens_out,
@@ -1239,6 +1299,7 @@ hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* to
   a.V = c.vocab;
   a.max_ctx = c.max_ctx;
   a.S = m.lay.mega_splits;
+  a.red_words = red_words(c, m.mega_blocks);
   a.eps = c.rms_eps;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
   const int blocks = m.mega_blocks;
