@@ -68,11 +68,17 @@ namespace {
 
 constexpr int kT = 512;          // threads per workgroup
 constexpr int kW = kT / AIO_WAVE; // waves per workgroup
-constexpr int kNLD = 8;          // 16-byte weight loads per lane per batch
+#ifndef AIO_STEP_NLD
+#define AIO_STEP_NLD 8
+#endif
+constexpr int kNLD = AIO_STEP_NLD;  // 16-byte weight loads per lane per batch
 // Batches in flight per wave (register buffers).  A deeper prefetch streams
 // the loops a little faster but delays the input poll queued behind it
 // (vector memory returns in order).
-constexpr int kNBUF = 2;
+#ifndef AIO_STEP_NBUF
+#define AIO_STEP_NBUF 2
+#endif
+constexpr int kNBUF = AIO_STEP_NBUF;
 constexpr unsigned kSpinLimit = 1u << 17;  // ~0.1-0.2 s of polling
 
 // s_waitcnt immediate for vmcnt(0) with expcnt and lgkmcnt left at their
@@ -363,6 +369,7 @@ template <int WFMT, int KIND, int VPL, int HD>
 AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[kNLD], const Thr& T) {
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
+  static_assert(UB >= 1, "a batch must hold at least one unit");
   const int lane = T.lane, wave = T.wave;
   const int ulast = P.nu - 1;
 #pragma unroll
@@ -377,33 +384,36 @@ AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[k
   }
 }
 
-// Reduce kNLD per-lane values over the 64 lanes of a wave.  Each halving
-// exchange (offsets 32, 16, 8) keeps half of the values, so lane l ends with
-// value (l >> 3) & 7 summed over 8 lanes; three plain exchanges finish the
-// sum (10 shuffles for 8 values instead of 48).
-AIO_DEV float reduce_rows(float (&v)[kNLD], int lane) {
-  static_assert(kNLD == 8, "reduce_rows assumes 8 values");
+// Reduce N per-lane values over the 64 lanes of a wave.  Each halving
+// exchange (offsets 32, 16, ...) keeps half of the values, so after log2 N
+// of them lane l holds value (l >> (6 - log2 N)) & (N - 1) summed over N
+// lanes; plain exchanges finish the sum within groups of 64 / N lanes
+// (10 shuffles for 8 values instead of 48).
+template <int N>
+constexpr int log2_of() { return N == 8 ? 3 : (N == 4 ? 2 : (N == 2 ? 1 : 0)); }
+
+// One halving exchange over lane bit OFF: values [0, HALF) keep the lower
+// or upper half of [0, 2 HALF) and add the partner's other half.
+template <int OFF, int HALF, int N>
+AIO_DEV void halve(float (&v)[N], int lane) {
+  const bool up = lane & OFF;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const bool up = lane & 32;
-    const float send = up ? v[i] : v[i + 4], keep = up ? v[i + 4] : v[i];
-    v[i] = keep + __shfl_xor(send, 32, AIO_WAVE);
+  for (int i = 0; i < HALF; ++i) {
+    const float send = up ? v[i] : v[i + HALF], keep = up ? v[i + HALF] : v[i];
+    v[i] = keep + __shfl_xor(send, OFF, AIO_WAVE);
   }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const bool up = lane & 16;
-    const float send = up ? v[i] : v[i + 2], keep = up ? v[i + 2] : v[i];
-    v[i] = keep + __shfl_xor(send, 16, AIO_WAVE);
-  }
-  {
-    const bool up = lane & 8;
-    const float send = up ? v[0] : v[1], keep = up ? v[1] : v[0];
-    v[0] = keep + __shfl_xor(send, 8, AIO_WAVE);
-  }
+}
+
+template <int N>
+AIO_DEV float reduce_rows(float (&v)[N], int lane) {
+  static_assert(N == 2 || N == 4 || N == 8, "reduce_rows takes 2, 4 or 8 values");
+  constexpr int LOG = log2_of<N>();
+  halve<32, N / 2>(v, lane);
+  if constexpr (N >= 4) halve<16, N / 4>(v, lane);
+  if constexpr (N >= 8) halve<8, 1>(v, lane);
   float s = v[0];
-  s += __shfl_xor(s, 4, AIO_WAVE);
-  s += __shfl_xor(s, 2, AIO_WAVE);
-  s += __shfl_xor(s, 1, AIO_WAVE);
+#pragma unroll
+  for (int off = 32 >> LOG; off >= 1; off >>= 1) s += __shfl_xor(s, off, AIO_WAVE);
   return s;
 }
 
@@ -436,9 +446,10 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
       t = dot4_i8(w.w, make_float4(h[v][12], h[v][13], h[v][14], h[v][15]), t);
     }
   }
-  const float s = reduce_rows(acc, lane);
-  const int idx = (lane >> 3) & 7;
-  if ((lane & 7) == 0 && idx < UB * RPU) {
+  const float s = reduce_rows<kNLD>(acc, lane);
+  constexpr int LOG = log2_of<kNLD>();
+  const int idx = (lane >> (6 - LOG)) & (kNLD - 1);
+  if ((lane & ((AIO_WAVE >> LOG) - 1)) == 0 && idx < UB * RPU) {
     const int ul = idx / RPU, r = idx % RPU;
     const int lu = batch * UB + ul;
     if (P.u0 + lu < P.u1) red[(lu * RPU + r) * kW + wave] = s;
@@ -610,16 +621,76 @@ AIO_DEV unsigned resid(const MegaArgs& a, int u) {
   return ld_dev((KIND == K_O ? a.xb : a.xa) + u);
 }
 
+// Epilogue inputs of this thread's first unit (u0 + tid) that do not depend
+// on this step's data: the RoPE cos/sin pairs at `pos` and the int8
+// per-channel scales.  They are requested when the phase starts, so the
+// epilogue does not wait a memory round trip for them after the loop.
+struct EpiPre {
+  float4 cs;      // QKV: (cos, sin) of dims i and i + 1
+  uint32_t s[2];  // int8 scales as fp16 bits: QKV two pairs, GU gate and up, else s[0]
+};
+
+// Position of QKV unit u: rotation dims i, i + 1 of a head, the matrix
+// (0 q, 1 k, 2 v) and the row of dim i in it.
+struct QkvRow {
+  int i, sec, rlo;
+};
+AIO_DEV QkvRow qkv_row(const MegaArgs& a, int u) {
+  const int half = a.hd / 2, qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+  const int p = 2 * u, head = p / half, i = p % half;  // pairs p, p+1 -> dims i, i+1
+  int sec = 0, rlo = head * a.hd + i;                   // virtual row of dim i
+  if (rlo >= qrows + krows) { sec = 2; rlo -= qrows + krows; }
+  else if (rlo >= qrows) { sec = 1; rlo -= qrows; }
+  return QkvRow{i, sec, rlo};
+}
+
+template <int WFMT, int KIND>
+AIO_DEV EpiPre epi_fetch(const MegaArgs& a, const GPhase& P, int pos, int u) {
+  EpiPre e;
+  e.cs = make_float4(0.f, 0.f, 0.f, 0.f);
+  e.s[0] = e.s[1] = 0u;
+  if constexpr (KIND == K_QKV) {
+    const QkvRow r = qkv_row(a, u);
+    const int half = a.hd / 2;
+    const u32x4 c = *(gl_u32x4*)(a.rope + (size_t)pos * half + r.i);
+    e.cs = make_float4(__uint_as_float(c.x), __uint_as_float(c.y), __uint_as_float(c.z),
+                       __uint_as_float(c.w));
+    if constexpr (WFMT == AIO_WFMT_INT8) {
+      const uint16_t* sc = pick3(r.sec, P.s0, P.s1, P.s2);
+      e.s[0] = *(const __attribute__((address_space(1))) uint32_t*)(sc + r.rlo);
+      e.s[1] = *(const __attribute__((address_space(1))) uint32_t*)(sc + r.rlo + half);
+    }
+  } else if constexpr (WFMT == AIO_WFMT_INT8) {
+    e.s[0] = *(const __attribute__((address_space(1))) uint16_t*)(P.s0 + u);
+    if constexpr (KIND == K_GU) e.s[1] = *(const __attribute__((address_space(1))) uint16_t*)(P.s1 + u);
+  }
+  return e;
+}
+
+AIO_DEV float fp16_lo(uint32_t w) { return fp16_to_f32((uint16_t)(w & 0xffffu)); }
+AIO_DEV float fp16_hi(uint32_t w) { return fp16_to_f32((uint16_t)(w >> 16)); }
+
 // Epilogue of a matrix phase: sum the kW wave partials of each row, then the
 // phase-specific output, stored with version `vo`.
 template <int WFMT, int KIND>
 AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, const float* red,
-                      Smem& sm, unsigned xpre, float inv, const Thr& T, unsigned vo, unsigned ep0) {
+                      Smem& sm, unsigned xpre, const EpiPre& pre, float inv, const Thr& T,
+                      unsigned vo, unsigned ep0) {
   constexpr int RPU = rpu_of<KIND>();
   const int nu = P.u1 - P.u0;
   const int tid = T.tid;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
+  // the layer's cache pointers, read as wave-uniform values: selected per
+  // lane from the table, they would come back through a vector load that
+  // waits behind every store and load in flight
+  uint16_t* kc = nullptr;
+  uint16_t* vc = nullptr;
+  if constexpr (KIND == K_QKV) {
+    const CMegaLayer* L = layer_at(a, layer);
+    kc = (uint16_t*)wave_uniform((const char*)L->kc);
+    vc = (uint16_t*)wave_uniform((const char*)L->vc);
+  }
   for (int t = tid; t < nu; t += kT) {
     float y[RPU];
 #pragma unroll
@@ -630,28 +701,26 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
       y[r] = KIND == K_O || KIND == K_DOWN ? s : s * inv;  // 1 / rms of a normed input
     }
     const int u = P.u0 + t;
+    // the prefetched epilogue inputs serve the first unit; a later one loads its own
+    const EpiPre e = t == tid ? pre : epi_fetch<WFMT, KIND>(a, P, pos, u);
     if constexpr (KIND == K_QKV) {
-      const int half = a.hd / 2, qrows = a.H * a.hd, krows = a.Hkv * a.hd;
-      const int p = 2 * u, head = p / half, i = p % half;  // pairs p, p+1 -> dims i, i+1
-      const int vlo = head * a.hd + i;                        // virtual row of dim i
-      int sec = 0, rlo = vlo;
-      if (vlo >= qrows + krows) { sec = 2; rlo -= qrows + krows; }
-      else if (vlo >= qrows) { sec = 1; rlo -= qrows; }
+      const int half = a.hd / 2;
+      const QkvRow qr = qkv_row(a, u);
+      const int sec = qr.sec, rlo = qr.rlo;
       // y[0] = dim i, y[1] = dim i+1, y[2] = dim i+half, y[3] = dim i+1+half
       if constexpr (WFMT == AIO_WFMT_INT8) {
-        const uint16_t* sc = pick3(sec, P.s0, P.s1, P.s2);
-        y[0] *= fp16_to_f32(sc[rlo]);
-        y[1] *= fp16_to_f32(sc[rlo + 1]);
-        y[2] *= fp16_to_f32(sc[rlo + half]);
-        y[3] *= fp16_to_f32(sc[rlo + 1 + half]);
+        y[0] *= fp16_lo(e.s[0]);
+        y[1] *= fp16_hi(e.s[0]);
+        y[2] *= fp16_lo(e.s[1]);
+        y[3] *= fp16_hi(e.s[1]);
       }
       if (sec < 2) {
+        const float c[2] = {e.cs.x, e.cs.z}, s[2] = {e.cs.y, e.cs.w};
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-          const float2 cs = a.rope[(size_t)pos * half + i + k];
           const float lo = y[k], hi = y[k + 2];
-          y[k] = lo * cs.x - hi * cs.y;
-          y[k + 2] = hi * cs.x + lo * cs.y;
+          y[k] = lo * c[k] - hi * s[k];
+          y[k + 2] = hi * c[k] + lo * s[k];
         }
       }
       if (sec == 0) {
@@ -661,8 +730,7 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         st_tag(a.q + rlo + half + 1, y[3], vo);
       } else {
         const int g = rlo / a.hd, ii = rlo % a.hd;
-        const CMegaLayer* L = layer_at(a, layer);
-        uint16_t* c = (sec == 1 ? L->kc : L->vc) + ((size_t)g * a.max_ctx + pos) * a.hd;
+        uint16_t* c = (sec == 1 ? kc : vc) + ((size_t)g * a.max_ctx + pos) * a.hd;
         const unsigned b0 = f32_to_bf16(y[0]), b1 = f32_to_bf16(y[1]);
         const unsigned b2 = f32_to_bf16(y[2]), b3 = f32_to_bf16(y[3]);
         st_dev((unsigned*)(c + ii), b0 | (b1 << 16));
@@ -677,13 +745,13 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
     } else if constexpr (KIND == K_GU) {
       float g = y[0], up = y[1];
       if constexpr (WFMT == AIO_WFMT_INT8) {
-        g *= fp16_to_f32(P.s0[u]);
-        up *= fp16_to_f32(P.s1[u]);
+        g *= fp16_lo(e.s[0]);
+        up *= fp16_lo(e.s[1]);
       }
       st_tag(a.m + u, g / (1.f + expf(-g)) * up, vo);
     } else {
       float yy = y[0];
-      if constexpr (WFMT == AIO_WFMT_INT8) yy *= fp16_to_f32(P.s0[u]);
+      if constexpr (WFMT == AIO_WFMT_INT8) yy *= fp16_lo(e.s[0]);
       if constexpr (KIND == K_LM) {
         a.logits[u] = yy;
         if (am_better(yy, u, bv, bi)) { bv = yy; bi = u; }
@@ -757,6 +825,11 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
     const int t = T.tid < P.u1 - P.u0 ? T.tid : 0;
     xpre = resid<KIND>(a, P.u0 + t < a.d ? P.u0 + t : a.d - 1);
   }
+  EpiPre pre;
+  {
+    const int t = T.tid < P.u1 - P.u0 ? T.tid : 0;
+    pre = epi_fetch<WFMT, KIND>(a, P, pos, P.u0 + t < P.nu ? P.u0 + t : P.nu - 1);
+  }
   // batch 0 is in flight (prefetch); then the input words, then the other
   // batches, so the wait for the input is queued behind one batch only
   // (the scheduling barriers keep the three groups of loads, and the first
@@ -795,7 +868,7 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
     for (int w = 0; w < kW; ++w) tot += ss8[w];
     inv = rsqrtf(tot / (float)P.K + a.eps);
   }
-  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, inv, T, ver_of(ep0, k), ep0);
+  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, pre, inv, T, ver_of(ep0, k), ep0);
   if (KIND != K_LM) {
     stamp(a.bar_arrive, k);
     if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
