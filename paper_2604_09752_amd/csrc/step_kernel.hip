@@ -870,6 +870,12 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
   }
   epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, pre, inv, T, ver_of(ep0, k), ep0);
   if (KIND != K_LM) {
+    // A workgroup's memory requests leave its CU in the order they were
+    // issued, by whatever wave.  The outputs are stored by the first waves
+    // only; without this barrier the other waves would already have queued
+    // the next phase's prefetch (tens of KB) in front of those stores, and
+    // every consumer would see them microseconds later.
+    __syncthreads();
     stamp(a.bar_arrive, k);
     if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
   }
@@ -986,24 +992,27 @@ AIO_DEV void load4(const AUnit& u, KV4& d, int t0) {
   }
 }
 
-// The first four keys of each group of this workgroup's first unit,
-// requested as soon as its QKV rows are out: the cached keys do not depend
-// on this step.  The next four follow the poll for q.
+// The first eight keys of each group of this workgroup's first unit (both
+// register sets), requested as soon as its QKV rows are out: the cached keys
+// do not depend on this step.  A workgroup's loads return in order and its
+// poll for q waits behind them, but the keys are needed before q is of any
+// use, so nothing is lost; requesting them earlier lets them arrive sooner.
 template <int HD>
-AIO_DEV void attn_prefetch(const MegaArgs& a, int layer, int pos, KV4& X) {
+AIO_DEV void attn_prefetch(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y) {
   const int units = a.Hkv * a.S;
   const int unit = (int)blockIdx.x < units ? (int)blockIdx.x : units - 1;
   const AUnit u = attn_unit<HD>(a, layer, unit, pos, thr());
   load4<HD>(u, X, 0);
+  load4<HD>(u, Y, 4);
 }
 
 // Merge the S split partials of kv head g (its G query heads) into o.
 // Thread (r, c) folds splits r, r + R, ... of output c with a running
 // log-sum-exp; the R partial folds then meet in LDS.  All loads of a thread
 // are issued before its first wait.
-template <int HD, int G>
+template <int HD, int G, int MS>
 AIO_DEV void attn_merge(const MegaArgs& a, int g, float* lds, unsigned ver) {
-  constexpr int NOUT = G * HD, R = kT / NOUT, MS = 16;
+  constexpr int NOUT = G * HD, R = kT / NOUT;
   const Thr T = thr();
   const int tid = T.tid, c = tid % NOUT, r = tid / NOUT, gg = c / HD, dim = c % HD;
   const int S = a.S;
@@ -1089,7 +1098,8 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
   const unsigned vq = ver_of(ep0, k - 1), vo = ver_of(ep0, k);
   for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
     const AUnit u = attn_unit<HD>(a, layer, unit, pos, T);
-    if (unit != (int)blockIdx.x) load4<HD>(u, X, 0);
+    const bool first = unit == (int)blockIdx.x;  // keys 0-7 already requested
+    if (!first) load4<HD>(u, X, 0);
     // q at this lane's 8 dims; in wave 0 of the last split also the new K/V row
     const unsigned* qb = a.q + (size_t)u.g * G * HD;
     int qoff[2 * G];
@@ -1116,7 +1126,7 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
       for (int i = 0; i < 4; ++i) nwd[i] = ld16_dev(nb, noff[i]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    load4<HD>(u, Y, 4);
+    if (!first) load4<HD>(u, Y, 4);
     __builtin_amdgcn_sched_barrier(0);
     await16(a, qb, qoff, qneed, qw, vq);
     if (unit == (int)blockIdx.x) stamp(a.bar_leave, k - 1);
@@ -1211,8 +1221,14 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
     __syncthreads();  // the LDS is reused by the next unit or the merge
   }
   stamp_detail(a, k, 0);
-  for (int g = 0; g < a.Hkv; ++g)
-    if ((g * S + S - 1) % (int)gridDim.x == (int)blockIdx.x) attn_merge<HD, G>(a, g, lds, vo);
+  // splits per merging thread (R threads per output): as many loads as
+  // there are splits to fold
+  for (int g = 0; g < a.Hkv; ++g) {
+    if ((g * S + S - 1) % (int)gridDim.x != (int)blockIdx.x) continue;
+    if (S <= 2 * R) attn_merge<HD, G, 2>(a, g, lds, vo);
+    else if (S <= 8 * R) attn_merge<HD, G, 8>(a, g, lds, vo);
+    else attn_merge<HD, G, 16>(a, g, lds, vo);
+  }
   stamp_detail(a, k, 1);
   stamp(a.bar_arrive, k);
   if (a.trace && blockIdx.x == 0 && threadIdx.x == 0) a.trace[k] = wall_clock64();
@@ -1239,7 +1255,7 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   for (int l = 0; l < a.L; ++l) {
     const unsigned k = 5u * (unsigned)l;
     gemv_phase<WFMT, HD, K_QKV, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 1);
-    attn_prefetch<HD>(a, l, pos, X);
+    attn_prefetch<HD>(a, l, pos, X, Y);
     attn_phase<HD, G>(a, l, pos, X, Y, lds + 2 * a.red_words, sm, ep0, k + 2);
     prefetch<WFMT, HD, K_O, VQ>(a, l, W);
     gemv_phase<WFMT, HD, K_O, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 3);
