@@ -90,6 +90,39 @@ def calibrate_copy(nbytes: int) -> int:
     return 0
 
 
+def pld_bench(dm, cfg, P, tau0, n, toks, logits) -> dict:
+    """Prompt-lookup decoding (host loop over aio_verify) against plain greedy
+    decoding of the same n tokens.  Random weights accept almost no drafts
+    from a random prompt, so the history is also given with the greedy
+    continuation planted behind a copy of its last two tokens and tau0: every
+    draft is then accepted.  The two runs bound PLD's speed on this model."""
+    import torch
+    import synth
+    k = min(cfg.verify_k, cfg.max_verify - 1)
+    prompt = [int(t) for t in synth.make_prompt(cfg)]
+    g = torch.zeros(n, dtype=torch.int32, device=dm.device)
+    dm.greedy(tau0, P, n, g, logits)
+    dm.sync()
+    t0 = time.perf_counter()
+    dm.greedy(tau0, P, n, g, logits)
+    dm.sync()
+    t_greedy = time.perf_counter() - t0
+    cont = [int(x) for x in g.cpu().numpy()]
+    j = 64
+    planted = prompt[:j] + [prompt[-2], prompt[-1], tau0] + cont + prompt[j + 3 + n:]
+    planted = planted[:P]
+    out = {"tokens": n, "k": k, "ngram": 3, "greedy_tokens_per_s": round(n / t_greedy, 2)}
+    for name, hist in (("random_prompt", prompt), ("planted_continuation", planted)):
+        dm.pld_generate(hist, P, tau0, min(n, 8), 3, 1, k)  # warm-up
+        t0 = time.perf_counter()
+        got, st = dm.pld_generate(hist, P, tau0, n, 3, 1, k)
+        dt = time.perf_counter() - t0
+        out[name] = {"tokens_per_s": round(n / dt, 2), "identical_to_greedy": bool(list(got) == cont),
+                     "acceptance": round(st["accepted"] / max(1, st["drafted"]), 3), **st}
+        log("pld %s: %.1f tokens/s (greedy %.1f), %s" % (name, n / dt, n / t_greedy, st))
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +133,9 @@ def main() -> int:
                     help="wall-clock budget of the oracle's CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3)
+    ap.add_argument("--pld", type=int, default=0, metavar="N",
+                    help="also time N tokens of prompt-lookup decoding (3-gram drafts, k = 8), "
+                         "with and without the greedy continuation planted in the history")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="instead of the decode bench, run a plain device-to-device copy of "
                          "BYTES (the reference kernel for HBM counter calibration) and exit")
@@ -240,6 +276,9 @@ def main() -> int:
         result["baseline_note"] = ("vs_baseline divides by the paper's 7B FP16 decode TPS at 2K "
                                    "(17.18, Ascend 910B, HF Transformers eager): context, "
                                    "another machine")
+
+    if args.pld > 0:
+        result["pld"] = pld_bench(dm, cfg, P, tau0, min(args.pld, cfg.max_ctx - P - 1), toks, logits)
 
     if not args.no_cpu_baseline:
         import oracle

@@ -224,6 +224,55 @@ int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_d
  * results are then invalid).  Synchronises. */
 int aio_device_status(aio_model* m, int32_t* status);
 
+/* ------------------------------------------ prompt-lookup decoding (host) */
+
+/* Prompt-lookup drafts: the draft source of PLD, which Section 3.3
+ * ("Dynamic Policy Routing and Execution", Strategy Routing) enables per
+ * request and Section 4.2 ("Models and Baselines", PLD Configuration)
+ * configures by an n-gram window and a look-ahead length.  Pure host
+ * function, no device work.  For n from min(ngram_max, n_hist - 1) down to
+ * ngram_min, looks for the last n tokens of hist[0..n_hist) earlier in hist;
+ * the earliest earlier occurrence that is followed by at least one token
+ * wins, and the up to k tokens that follow it are the drafts.  drafts (host,
+ * k int32) receives them and *n_drafts their count (0 when no n-gram
+ * recurs).
+ * AIO_EINVAL: a null pointer.  AIO_ERANGE: n_hist < 0, k < 0, ngram_min < 1
+ * or ngram_max < ngram_min. */
+int aio_pld_match(const int32_t* hist, int32_t n_hist, int32_t ngram_max, int32_t ngram_min,
+                  int32_t k, int32_t* drafts, int32_t* n_drafts);
+
+typedef struct aio_pld_stats {
+  int32_t forwards; /* model forwards: verify calls plus single decode steps */
+  int32_t verifies; /* forwards that scored drafts                          */
+  int32_t drafted;  /* draft tokens scored                                  */
+  int32_t accepted; /* draft tokens accepted                                */
+} aio_pld_stats;
+
+/* Greedy generation with prompt-lookup decoding (Section 3.3, Strategy
+ * Routing; Section 4.2, PLD Configuration).  history (host, pos int32) holds
+ * the tokens at positions 0..pos-1, whose K/V the cache already holds;
+ * `token` is consumed at pos.  Each round drafts up to k tokens with
+ * aio_pld_match over everything consumed so far plus `token` (never more
+ * drafts than tokens still wanted, nor past the end of the cache), scores
+ * [token, drafts] in one aio_verify (or one aio_decode_step when nothing
+ * matches), takes each row's greedy argmax on the device, and accepts the
+ * longest prefix of drafts in which every draft equals the argmax of the row
+ * before it.  The argmax of the row after the last accepted draft is the
+ * next token, consumed by the next round at pos + accepted + 1 (cache rows
+ * written past that are overwritten later, never read).  out (host, n_new
+ * int32) receives the generated tokens; they are the tokens plain greedy
+ * decoding produces from the same state, whatever the acceptance.
+ * logits_dev (fp32 [k+1][vocab], 16-byte aligned) and argmax_dev (int32
+ * [k+1]) are scratch.  stats may be NULL.  Synchronises the model's stream
+ * once per round and returns when all n_new tokens are generated.
+ * AIO_ERANGE: token outside [0, vocab), pos < 0, n_new < 1,
+ * pos + n_new > max_ctx, k < 0, k + 1 > max_verify, ngram_min < 1 or
+ * ngram_max < ngram_min.  AIO_EINVAL: a null pointer or a history token
+ * outside [0, vocab). */
+int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t token,
+                     int32_t n_new, int32_t ngram_max, int32_t ngram_min, int32_t k,
+                     float* logits_dev, int32_t* argmax_dev, int32_t* out, aio_pld_stats* stats);
+
 #ifdef __cplusplus
 }
 #endif

@@ -39,6 +39,11 @@ class aio_weights(ctypes.Structure):
                 ("layers", ctypes.POINTER(aio_layer_weights))]
 
 
+class aio_pld_stats(ctypes.Structure):
+    _fields_ = [("forwards", ctypes.c_int32), ("verifies", ctypes.c_int32),
+                ("drafted", ctypes.c_int32), ("accepted", ctypes.c_int32)]
+
+
 class AioError(RuntimeError):
     def __init__(self, code: int, what: str):
         self.code = code
@@ -81,6 +86,9 @@ def lib():
         L.aio_device_status.argtypes = [vp, P(i32)]
         L.aio_trace_barriers.argtypes = [vp, i32, i32, vp, vp, vp, i32, P(i32), P(i32)]
         L.aio_uses_step_kernel.argtypes = [vp]
+        L.aio_pld_match.argtypes = [vp, i32, i32, i32, i32, vp, P(i32)]
+        L.aio_pld_generate.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp,
+                                       P(aio_pld_stats)]
         _lib = L
     return _lib
 
@@ -213,6 +221,31 @@ def aio_trace_barriers(handle: int, token: int, pos: int, logits: torch.Tensor, 
     return arr[:n].reshape(nb.value, nk.value), lev[:n].reshape(nb.value, nk.value)
 
 
+def aio_pld_match(hist, ngram_max: int, ngram_min: int, k: int) -> np.ndarray:
+    """Prompt-lookup drafts for the history ``hist`` (pure host call)."""
+    h = np.ascontiguousarray(hist, dtype=np.int32)
+    out = np.zeros(max(int(k), 1), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib().aio_pld_match(h.ctypes.data if h.size else None, int(h.size), int(ngram_max),
+                               int(ngram_min), int(k), out.ctypes.data, ctypes.byref(n)),
+           "aio_pld_match")
+    return out[: n.value].copy()
+
+
+def aio_pld_generate(handle: int, history, pos: int, token: int, n_new: int, ngram_max: int,
+                     ngram_min: int, k: int, logits: torch.Tensor, argmax_out: torch.Tensor):
+    """Greedy generation with prompt-lookup decoding; returns (tokens, stats)."""
+    h = np.ascontiguousarray(history, dtype=np.int32)
+    assert h.size == pos
+    out = np.zeros(int(n_new), dtype=np.int32)
+    st = aio_pld_stats()
+    _check(lib().aio_pld_generate(handle, h.ctypes.data if h.size else None, int(pos), int(token),
+                                  int(n_new), int(ngram_max), int(ngram_min), int(k),
+                                  _ptr(logits), _ptr(argmax_out), out.ctypes.data,
+                                  ctypes.byref(st)), "aio_pld_generate")
+    return out, {f: int(getattr(st, f)) for f, _ in aio_pld_stats._fields_}
+
+
 def aio_device_status(handle: int) -> int:
     st = ctypes.c_int32(0)
     _check(lib().aio_device_status(handle, ctypes.byref(st)), "aio_device_status")
@@ -299,6 +332,14 @@ class DeviceModel:
     def greedy(self, token: int, pos: int, n_steps: int, tokens: torch.Tensor,
                logits: torch.Tensor) -> None:
         aio_decode_greedy(self.handle, token, pos, n_steps, tokens, logits)
+
+    def pld_generate(self, history, pos: int, token: int, n_new: int, ngram_max: int,
+                     ngram_min: int, k: int):
+        """Prompt-lookup greedy generation of n_new tokens (synchronous)."""
+        logits = self.new_logits(k + 1)
+        am = torch.zeros(k + 1, dtype=torch.int32, device=self.device)
+        return aio_pld_generate(self.handle, history, pos, token, n_new, ngram_max, ngram_min, k,
+                                logits, am)
 
     def profile_step(self, token: int, pos: int, logits: torch.Tensor) -> np.ndarray:
         return aio_profile_step(self.handle, token, pos, logits, 6 * self.c.n_layers + 1)

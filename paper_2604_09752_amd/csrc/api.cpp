@@ -4,6 +4,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <string>
 #include <vector>
@@ -474,5 +475,79 @@ int aio_device_status(aio_model* m, int32_t* status) {
 }
 
 int aio_uses_step_kernel(const aio_model* m) { return m && m->use_mega ? 1 : 0; }
+
+// ------------------------------------------------- prompt-lookup decoding
+
+int aio_pld_match(const int32_t* hist, int32_t n_hist, int32_t ngram_max, int32_t ngram_min,
+                  int32_t k, int32_t* drafts, int32_t* n_drafts) {
+  if (!n_drafts || (n_hist > 0 && !hist) || (k > 0 && !drafts)) return AIO_EINVAL;
+  if (n_hist < 0 || k < 0 || ngram_min < 1 || ngram_max < ngram_min) return AIO_ERANGE;
+  *n_drafts = 0;
+  if (k == 0) return AIO_OK;
+  // largest n-gram first; within one n, the earliest occurrence with a
+  // continuation (the suffix itself starts at n_hist - n and has none)
+  for (int n = std::min(ngram_max, n_hist - 1); n >= ngram_min; --n) {
+    const int32_t* suffix = hist + (n_hist - n);
+    for (int i = 0; i + n < n_hist; ++i) {
+      if (!std::equal(suffix, suffix + n, hist + i)) continue;
+      const int cnt = std::min(k, n_hist - (i + n));
+      std::copy(hist + i + n, hist + i + n + cnt, drafts);
+      *n_drafts = cnt;
+      return AIO_OK;
+    }
+  }
+  return AIO_OK;
+}
+
+int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t token,
+                     int32_t n_new, int32_t ngram_max, int32_t ngram_min, int32_t k,
+                     float* logits_dev, int32_t* argmax_dev, int32_t* out, aio_pld_stats* stats) {
+  if (!m || !logits_dev || !aligned16(logits_dev) || !argmax_dev || !out) return AIO_EINVAL;
+  if (((uintptr_t)argmax_dev & 3u) || (pos > 0 && !history)) return AIO_EINVAL;
+  const aio_config& c = m->cfg;
+  if (token < 0 || token >= c.vocab || pos < 0 || n_new < 1 || k < 0 || k + 1 > c.max_verify ||
+      ngram_min < 1 || ngram_max < ngram_min)
+    return AIO_ERANGE;
+  if ((int64_t)pos + n_new > c.max_ctx) return AIO_ERANGE;
+  for (int32_t i = 0; i < pos; ++i)
+    if (history[i] < 0 || history[i] >= c.vocab) return AIO_EINVAL;
+  std::vector<int32_t> hist(history, history + pos);
+  hist.reserve((size_t)pos + (size_t)n_new + 1);
+  hist.push_back(token);
+  aio_pld_stats st{};
+  int32_t drafts[AIO_MAX_VERIFY_ROWS], y[AIO_MAX_VERIFY_ROWS];
+  int32_t p = pos, t = token, made = 0;
+  while (made < n_new) {
+    const int kk = std::min(std::min(k, n_new - made - 1), c.max_ctx - 1 - p);
+    int32_t nd = 0;
+    if (kk > 0) {
+      const int rc = aio_pld_match(hist.data(), (int32_t)hist.size(), ngram_max, ngram_min, kk,
+                                   drafts, &nd);
+      if (rc) return rc;
+    }
+    int rc = nd > 0 ? aio_verify(m, t, drafts, nd, p, logits_dev)
+                    : aio_decode_step(m, t, p, logits_dev);
+    if (rc) return rc;
+    if ((rc = aio_argmax(m, logits_dev, nd + 1, c.vocab, argmax_dev))) return rc;
+    hipError_t e = hipMemcpyAsync(y, argmax_dev, (size_t)(nd + 1) * sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return hip_fail(e);
+    int a = 0;
+    while (a < nd && drafts[a] == y[a]) ++a;  // row a's argmax follows drafts[0..a)
+    st.forwards += 1;
+    st.verifies += nd > 0;
+    st.drafted += nd;
+    st.accepted += a;
+    for (int i = 0; i <= a && made < n_new; ++i) {
+      out[made++] = y[i];
+      hist.push_back(y[i]);
+    }
+    p += a + 1;
+    t = y[a];
+  }
+  if (stats) *stats = st;
+  return AIO_OK;
+}
 
 }  // extern "C"
