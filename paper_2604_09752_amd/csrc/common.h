@@ -75,3 +75,24 @@ AIO_DEV float dot4_i8(uint32_t w, const float4 a, float acc) {
   acc = fmaf(i8_at(w, 3), a.w, acc);
   return acc;
 }
+
+// One DPP lane move of a float (a VALU operation: no LDS round trip).
+template <int CTRL>
+AIO_DEV float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of 8 or 16 lanes; every lane of a group receives
+// the same total.  Each step adds a lane's value to that of a partner in the
+// other half of its current group: lane ^ 1, lane ^ 2 (quad permutations),
+// then the mirror lane of the other quad (row_half_mirror) and, for 16, of
+// the other half row (row_mirror).
+template <int WIDTH>
+AIO_DEV float group_sum_dpp(float v) {
+  static_assert(WIDTH == 8 || WIDTH == 16, "DPP sums cover 8 or 16 lanes");
+  v += dpp_mov<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  if (WIDTH == 16) v += dpp_mov<0x140>(v);  // row_mirror
+  return v;
+}

@@ -25,6 +25,10 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / AIO_WAVE;
+// The skinny GEMM runs 8 waves per workgroup: more weight loads in flight
+// per CU, and the K range of a workgroup split eight ways.
+constexpr int kGBlock = 512;
+constexpr int kGWaves = kGBlock / AIO_WAVE;
 constexpr int kMaxRows = AIO_MAX_VERIFY_ROWS;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -106,14 +110,24 @@ struct VGemmArgs {
   const float2* rope;
   const aio_state* st;
   int H, Hkv, hd, max_ctx;
+  int ks;                   // K splits across workgroups (grid.y); > 1 only for EPI_RESID
 };
 
-// 16 consecutive k of one weight row as two bf16x8 MFMA fragments.
+// Two bf16x8 MFMA fragments of one weight row in a block of 32 k: for bf16,
+// k .. k+7 and k+16 .. k+23 (k = block + 8 kh, so that the two lanes of a
+// row read 32 adjacent bytes per load); for int8, the 16 consecutive k from
+// k (k = block + 16 kh, one 16-byte load).  The activation fragments use
+// the same k (vk_lo, vk_hi).
+template <int WFMT>
+AIO_DEV int vk_lo(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 8 * kh : block + 16 * kh; }
+template <int WFMT>
+AIO_DEV int vk_hi(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 16 + 8 * kh : block + 16 * kh + 8; }
+
 template <int WFMT>
 AIO_DEV void load_a(const char* row, int k, bf16x8& lo, bf16x8& hi) {
   if constexpr (WFMT == AIO_WFMT_BF16) {
     const uint4* p = (const uint4*)(row + (size_t)k * 2);
-    const uint4 u0 = ld_stream(p), u1 = ld_stream(p + 1);
+    const uint4 u0 = ld_stream(p), u1 = ld_stream(p + 2);
     lo = __builtin_bit_cast(bf16x8, u0);
     hi = __builtin_bit_cast(bf16x8, u1);
   } else {
@@ -134,16 +148,45 @@ AIO_DEV void load_a(const char* row, int k, bf16x8& lo, bf16x8& hi) {
   }
 }
 
-// Each workgroup owns T = 2 tiles of 32 output channels; its 4 waves split
-// K into quarters and their partial 32x32 tiles are summed in LDS.  Lane l
-// of a wave covers weight row (l % 32) of each tile and, in a block of 32 k,
-// the 16 consecutive k starting at 16 * (l / 32); MFMA "a" takes the first 8
-// and MFMA "b" the next 8, and the B operand (activation column l % 32) is
-// loaded with the same k mapping, so the k permutation cancels.
+// Each workgroup owns T = 2 tiles of 32 output channels and one of a.ks
+// slices of K (grid.y); its 8 waves split the slice and their partial 32x32
+// tiles are summed in LDS.  Lane l of a wave covers weight row (l % 32) of
+// each tile and, in a block of 32 k, 16 of the k (load_a gives which); MFMA
+// "a" takes 8 of them and MFMA "b" the other 8, and the B operand
+// (activation column l % 32) is loaded with the same k mapping, so the k
+// permutation cancels.  Blocks of k stream through two register sets: the
+// loads of block i + 2 are issued as soon as block i is multiplied.
+template <int WFMT, int T>
+struct VFrag {
+  bf16x8 wa[T], wb[T], ba, bb;
+};
+
+template <int WFMT, int T>
+AIO_DEV void vload(VFrag<WFMT, T>& f, const char* const (&rowp)[T], const uint16_t* actp,
+                   int block, int kh) {
+  const int klo = vk_lo<WFMT>(block, kh), khi = vk_hi<WFMT>(block, kh);
+#pragma unroll
+  for (int t = 0; t < T; ++t) load_a<WFMT>(rowp[t], klo, f.wa[t], f.wb[t]);
+  f.ba = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + klo));
+  f.bb = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + khi));
+}
+
+template <int WFMT, int T>
+AIO_DEV void vmma(const VFrag<WFMT, T>& f, bool col_live, f32x16 (&acc)[T]) {
+  // dead columns (past the 3M split terms) multiply zeros
+  const bf16x8 z = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+  const bf16x8 ba = col_live ? f.ba : z, bb = col_live ? f.bb : z;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.wa[t], ba, acc[t], 0, 0, 0);
+    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.wb[t], bb, acc[t], 0, 0, 0);
+  }
+}
+
 template <int WFMT, int EPI>
-__global__ __launch_bounds__(kBlock) void k_vgemm(VGemmArgs a) {
+__global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   constexpr int T = 2;
-  __shared__ float red[kWaves][T][32][33];
+  __shared__ float red[kGWaves / 2][T][32][33];
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
   const int rl = lane & 31, kh = lane >> 5;
   const size_t wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
@@ -181,55 +224,80 @@ __global__ __launch_bounds__(kBlock) void k_vgemm(VGemmArgs a) {
     rowp[t] = (const char*)tile_w[t] + (size_t)n * a.K * wbytes;
   }
   const bool col_live = rl < 3 * a.M;
-  const uint16_t* actp = a.act + (size_t)rl * a.lda;
+  // dead columns read row 0 (in bounds) and are zeroed before the product
+  const uint16_t* actp = a.act + (size_t)(col_live ? rl : 0) * a.lda;
 
+  // Blocks of 32 k of this workgroup's K slice, dealt to the waves in turn
+  // (wave w takes blocks w, w + 8, ...): at any moment the eight waves read
+  // adjacent stretches of the same rows, which keeps HBM pages open.
   const int nkb = a.K / 32;
-  const int kb0 = wid * nkb / kWaves, kb1 = (wid + 1) * nkb / kWaves;
+  const int ks = (int)blockIdx.y;
+  const int kbA = ks * nkb / a.ks, kbB = (ks + 1) * nkb / a.ks;
+  const int nk = kbB - kbA;
+  const int nw = nk > wid ? (nk - wid + kGWaves - 1) / kGWaves : 0;  // this wave's blocks
   f32x16 acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
 
-  for (int kb = kb0; kb < kb1; ++kb) {
-    const int k = kb * 32 + kh * 16;
-    bf16x8 wa[T], wb[T];
-#pragma unroll
-    for (int t = 0; t < T; ++t) load_a<WFMT>(rowp[t], k, wa[t], wb[t]);
-    bf16x8 ba, bb;
-    if (col_live) {
-      const uint4* ap = (const uint4*)(actp + k);
-      ba = __builtin_bit_cast(bf16x8, ap[0]);
-      bb = __builtin_bit_cast(bf16x8, ap[1]);
-    } else {
-      ba = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
-      bb = ba;
+  if (nw > 0) {
+    // loads past the wave's last block re-read that block (same lines) and
+    // are never multiplied
+    auto kof = [&](int i) { return (kbA + wid + (i < nw ? i : nw - 1) * kGWaves) * 32; };
+    VFrag<WFMT, T> f0, f1;
+    vload(f0, rowp, actp, kof(0), kh);
+    vload(f1, rowp, actp, kof(1), kh);
+    int i = 0;
+    // the scheduling barriers keep each set's loads right after its products:
+    // left to itself the compiler hoists all loads of an iteration to its
+    // top and then waits for every one of them
+    for (; i + 2 < nw; i += 2) {
+      vmma(f0, col_live, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      vload(f0, rowp, actp, kof(i + 2), kh);
+      __builtin_amdgcn_sched_barrier(0);
+      vmma(f1, col_live, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      vload(f1, rowp, actp, kof(i + 3), kh);
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[t], ba, acc[t], 0, 0, 0);
-      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[t], bb, acc[t], 0, 0, 0);
-    }
+    vmma(f0, col_live, acc);
+    if (i + 1 < nw) vmma(f1, col_live, acc);
   }
   // D layout: lane l, register v -> column j = l % 32,
-  // row i = 8 * (v / 4) + 4 * (l / 32) + (v % 4).
+  // row i = 8 * (v / 4) + 4 * (l / 32) + (v % 4).  The upper four waves
+  // hand their tiles to the lower four, which then write the sums.
+  if (wid >= kGWaves / 2) {
 #pragma unroll
-  for (int t = 0; t < T; ++t)
+    for (int t = 0; t < T; ++t)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) red[wid][t][8 * (v / 4) + 4 * kh + (v % 4)][rl] = acc[t][v];
+      for (int v = 0; v < 16; ++v)
+        red[wid - kGWaves / 2][t][8 * (v / 4) + 4 * kh + (v % 4)][rl] = acc[t][v];
+  }
+  __syncthreads();
+  if (wid < kGWaves / 2) {
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float& r = red[wid][t][8 * (v / 4) + 4 * kh + (v % 4)][rl];
+        r += acc[t][v];
+      }
+  }
   __syncthreads();
 
-  // Sum the four K quarters and the three split terms: y[r][i] for the tile.
+  // Sum the four wave pairs and the three split terms: y[r][i] for the tile.
   const int M = a.M;
   const int pos = a.st->pos;
-  for (int e = tid; e < 32 * M; e += kBlock) {
+  for (int e = tid; e < 32 * M; e += kGBlock) {
     const int i = e % 32, r = e / 32;
     float y[T];
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       float s = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w)
+      for (int w = 0; w < kGWaves / 2; ++w)
         s += red[w][t][i][r] + red[w][t][i][M + r] + red[w][t][i][2 * M + r];
       y[t] = s;
     }
@@ -285,8 +353,13 @@ __global__ __launch_bounds__(kBlock) void k_vgemm(VGemmArgs a) {
         if (n >= a.N) continue;
         float v = y[t];
         if constexpr (WFMT == AIO_WFMT_INT8) v *= fp16_to_f32(a.s0[n]);
-        if constexpr (EPI == EPI_RESID) a.out[(size_t)r * a.ldo + n] += v;
-        else a.out[(size_t)r * a.ldo + n] = v;
+        if constexpr (EPI == EPI_RESID) {
+          // K split over workgroups: each adds its part of the product
+          if (a.ks > 1) unsafeAtomicAdd(a.out + (size_t)r * a.ldo + n, v);
+          else a.out[(size_t)r * a.ldo + n] += v;
+        } else {
+          a.out[(size_t)r * a.ldo + n] = v;
+        }
       }
     }
   }
@@ -333,20 +406,36 @@ __global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
   }
   const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD + li * 8;
   const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD + li * 8;
-  for (int j = j0 + gi; j < j1; j += NG) {
-    const uint4 kk = *(const uint4*)(kbase + (size_t)j * HD);
-    const uint4 vv = *(const uint4*)(vbase + (size_t)j * HD);
-    const float vf[8] = {bf16_lo(vv.x), bf16_hi(vv.x), bf16_lo(vv.y), bf16_hi(vv.y),
-                         bf16_lo(vv.z), bf16_hi(vv.z), bf16_lo(vv.w), bf16_hi(vv.w)};
+  // four keys per group are requested before any is used (a key past the
+  // split reads the split's first row and is masked), then each is scored
+  // against every row with a DPP sum over the group's lanes
+  for (int j = j0 + gi; j < j1; j += 4 * NG) {
+    uint4 kk[4], vv[4];
+    bool valid[4];
 #pragma unroll
-    for (int r = 0; r < kMaxRows; ++r) {
-      if (r < M) {
-        float sc = dot8_bf16(kk, make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
-                             make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f);
-        sc = group_sum<LPK>(sc);
-        if (j <= pos + r) {  // causal: row r sees keys [0, pos + r]
-          const float mn = fmaxf(m[r], sc);
-          const float c = exp2f(m[r] - mn), p = exp2f(sc - mn);
+    for (int u = 0; u < 4; ++u) {
+      const int jj = j + u * NG;
+      valid[u] = jj < j1;
+      const size_t off = (size_t)(valid[u] ? jj : j0) * HD;
+      kk[u] = *(const uint4*)(kbase + off);
+      vv[u] = *(const uint4*)(vbase + off);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int jj = j + u * NG;
+      const float vf[8] = {bf16_lo(vv[u].x), bf16_hi(vv[u].x), bf16_lo(vv[u].y), bf16_hi(vv[u].y),
+                           bf16_lo(vv[u].z), bf16_hi(vv[u].z), bf16_lo(vv[u].w), bf16_hi(vv[u].w)};
+#pragma unroll
+      for (int r = 0; r < kMaxRows; ++r) {
+        if (r < M) {
+          float sc = dot8_bf16(kk[u], make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
+                               make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f);
+          sc = group_sum_dpp<LPK>(sc);
+          // causal: row r sees keys [0, pos + r]; masked keys leave the state
+          const bool take = valid[u] && jj <= pos + r;
+          const float mn = take ? fmaxf(m[r], sc) : m[r];
+          const float c = take ? exp2f(m[r] - mn) : 1.f;
+          const float p = take ? exp2f(sc - mn) : 0.f;
           l[r] = l[r] * c + p;
 #pragma unroll
           for (int i = 0; i < 8; ++i) o[r][i] = fmaf(p, vf[i], o[r][i] * c);
@@ -419,12 +508,22 @@ __global__ __launch_bounds__(128) void k_vmerge(VMergeArgs a) {
   }
 }
 
+// Launch with `blocks` tile pairs.  A residual-add product with fewer tile
+// pairs than CUs also splits K over workgroups, as far as every wave keeps
+// at least two blocks of 32 k; the others run one K slice per workgroup.
 template <int EPI>
-hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& a, int blocks) {
+hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
+  VGemmArgs a = g;
+  a.ks = 1;
+  if (EPI == EPI_RESID) {
+    const int nkb = a.K / 32;
+    while (blocks * a.ks < m.num_cus && nkb / (2 * a.ks * kGWaves) >= 2) a.ks *= 2;
+  }
+  const dim3 grid(blocks, a.ks);
   if (m.cfg.wfmt == AIO_WFMT_INT8)
-    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), dim3(blocks), dim3(kBlock), 0, m.stream, a);
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), grid, dim3(kGBlock), 0, m.stream, a);
   else
-    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), dim3(blocks), dim3(kBlock), 0, m.stream, a);
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), grid, dim3(kGBlock), 0, m.stream, a);
   return hipGetLastError();
 }
 
