@@ -113,25 +113,41 @@ struct VGemmArgs {
   int ks;                   // K splits across workgroups (grid.y); > 1 only for EPI_RESID
 };
 
-// Two bf16x8 MFMA fragments of one weight row in a block of 32 k: for bf16,
-// k .. k+7 and k+16 .. k+23 (k = block + 8 kh, so that the two lanes of a
-// row read 32 adjacent bytes per load); for int8, the 16 consecutive k from
-// k (k = block + 16 kh, one 16-byte load).  The activation fragments use
-// the same k (vk_lo, vk_hi).
+// The k of the two MFMA fragments a lane holds in a block of 32 k (lane
+// half kh = l / 32): for bf16, k .. k+7 and k+16 .. k+23 from block + 8 kh;
+// for int8, the 16 consecutive k from block + 16 kh.  Weights (frag_lds)
+// and activations use the same k, so the permutation cancels.
 template <int WFMT>
 AIO_DEV int vk_lo(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 8 * kh : block + 16 * kh; }
 template <int WFMT>
 AIO_DEV int vk_hi(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 16 + 8 * kh : block + 16 * kh + 8; }
 
+// Weights reach the MFMA through LDS in stages of 256 k.  Read straight
+// into the MFMA operand layout, every load instruction would span 32 rows at
+// 16-32 bytes each; staged, one wave instruction reads 512 (bf16) or 256
+// (int8) contiguous bytes of each of 2 or 4 rows, and the 64 rows of a stage
+// go to LDS with a 16-byte skew per row, so that the fragment reads (32 rows
+// at one column) fall in distinct banks.
 template <int WFMT>
-AIO_DEV void load_a(const char* row, int k, bf16x8& lo, bf16x8& hi) {
+struct VStage {
+  static constexpr int KC = 256;                                     // k per stage
+  static constexpr int RB = KC * (WFMT == AIO_WFMT_BF16 ? 2 : 1);    // bytes of a row
+  static constexpr int RS = RB + 16;                                 // LDS row stride
+  static constexpr int CPR = RB / 16;                                // 16-byte chunks per row
+  static constexpr int NLD = 64 * CPR / kGBlock;                     // loads per thread
+  static constexpr int BYTES = 64 * RS;
+};
+
+// Two bf16x8 MFMA fragments of one staged row for the wave's block of 32 k
+// (the same k as vk_lo / vk_hi give for the activations).
+template <int WFMT>
+AIO_DEV void frag_lds(const char* rowl, int wblock, int kh, bf16x8& lo, bf16x8& hi) {
   if constexpr (WFMT == AIO_WFMT_BF16) {
-    const uint4* p = (const uint4*)(row + (size_t)k * 2);
-    const uint4 u0 = ld_stream(p), u1 = ld_stream(p + 2);
-    lo = __builtin_bit_cast(bf16x8, u0);
-    hi = __builtin_bit_cast(bf16x8, u1);
+    const char* p = rowl + (size_t)(wblock * 32 + 8 * kh) * 2;
+    lo = __builtin_bit_cast(bf16x8, *(const uint4*)p);
+    hi = __builtin_bit_cast(bf16x8, *(const uint4*)(p + 32));
   } else {
-    const uint4 u = ld_stream((const uint4*)(row + k));
+    const uint4 u = *(const uint4*)(rowl + wblock * 32 + 16 * kh);
     uint32_t w[4] = {u.x, u.y, u.z, u.w};
     uint32_t o[8];
 #pragma unroll
@@ -149,27 +165,17 @@ AIO_DEV void load_a(const char* row, int k, bf16x8& lo, bf16x8& hi) {
 }
 
 // Each workgroup owns T = 2 tiles of 32 output channels and one of a.ks
-// slices of K (grid.y); its 8 waves split the slice and their partial 32x32
-// tiles are summed in LDS.  Lane l of a wave covers weight row (l % 32) of
-// each tile and, in a block of 32 k, 16 of the k (load_a gives which); MFMA
-// "a" takes 8 of them and MFMA "b" the other 8, and the B operand
-// (activation column l % 32) is loaded with the same k mapping, so the k
-// permutation cancels.  Blocks of k stream through two register sets: the
-// loads of block i + 2 are issued as soon as block i is multiplied.
+// slices of K (grid.y).  Its weights pass through LDS in stages (VStage),
+// two stages in flight in registers; wave w multiplies block w of every
+// stage, and the 8 waves' partial 32x32 tiles are summed in LDS at the end.
+// Lane l of a wave covers tile row (l % 32) and 16 of the 32 k of a block
+// (vk_lo, vk_hi): MFMA "a" takes 8 of them and MFMA "b" the other 8; the B
+// operand (activation column l % 32) is loaded with the same k, so the k
+// permutation cancels.
 template <int WFMT, int T>
 struct VFrag {
   bf16x8 wa[T], wb[T], ba, bb;
 };
-
-template <int WFMT, int T>
-AIO_DEV void vload(VFrag<WFMT, T>& f, const char* const (&rowp)[T], const uint16_t* actp,
-                   int block, int kh) {
-  const int klo = vk_lo<WFMT>(block, kh), khi = vk_hi<WFMT>(block, kh);
-#pragma unroll
-  for (int t = 0; t < T; ++t) load_a<WFMT>(rowp[t], klo, f.wa[t], f.wb[t]);
-  f.ba = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + klo));
-  f.bb = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + khi));
-}
 
 template <int WFMT, int T>
 AIO_DEV void vmma(const VFrag<WFMT, T>& f, bool col_live, f32x16 (&acc)[T]) {
@@ -186,7 +192,11 @@ AIO_DEV void vmma(const VFrag<WFMT, T>& f, bool col_live, f32x16 (&acc)[T]) {
 template <int WFMT, int EPI>
 __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   constexpr int T = 2;
-  __shared__ float red[kGWaves / 2][T][32][33];
+  using St = VStage<WFMT>;
+  constexpr int kRedBytes = (int)sizeof(float) * (kGWaves / 2) * T * 32 * 33;
+  // the weight stage during the product, then the partial tiles
+  __shared__ __align__(16) char smem[St::BYTES > kRedBytes ? St::BYTES : kRedBytes];
+  float (*red)[T][32][33] = (float (*)[T][32][33])smem;
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
   const int rl = lane & 31, kh = lane >> 5;
   const size_t wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
@@ -216,55 +226,90 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
     tile_w[0] = tile_w[1] = a.w0;
   }
   const int n_rows_w = (EPI == EPI_QKV) ? 0 : a.N;  // clamp bound for plain tiles
-  const char* rowp[T];
-#pragma unroll
-  for (int t = 0; t < T; ++t) {
-    int n = tile_row[t] + rl;
-    if (n_rows_w && n >= n_rows_w) n = n_rows_w - 1;
-    rowp[t] = (const char*)tile_w[t] + (size_t)n * a.K * wbytes;
-  }
   const bool col_live = rl < 3 * a.M;
   // dead columns read row 0 (in bounds) and are zeroed before the product
   const uint16_t* actp = a.act + (size_t)(col_live ? rl : 0) * a.lda;
 
-  // Blocks of 32 k of this workgroup's K slice, dealt to the waves in turn
-  // (wave w takes blocks w, w + 8, ...): at any moment the eight waves read
-  // adjacent stretches of the same rows, which keeps HBM pages open.
+  // This workgroup's K slice in stages of 8 blocks of 32 k; wave w
+  // multiplies block w of every stage.
   const int nkb = a.K / 32;
   const int ks = (int)blockIdx.y;
   const int kbA = ks * nkb / a.ks, kbB = (ks + 1) * nkb / a.ks;
-  const int nk = kbB - kbA;
-  const int nw = nk > wid ? (nk - wid + kGWaves - 1) / kGWaves : 0;  // this wave's blocks
+  const int nst = (kbB - kbA + 7) / 8;
   f32x16 acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
 
-  if (nw > 0) {
-    // loads past the wave's last block re-read that block (same lines) and
-    // are never multiplied
-    auto kof = [&](int i) { return (kbA + wid + (i < nw ? i : nw - 1) * kGWaves) * 32; };
-    VFrag<WFMT, T> f0, f1;
-    vload(f0, rowp, actp, kof(0), kh);
-    vload(f1, rowp, actp, kof(1), kh);
-    int i = 0;
-    // the scheduling barriers keep each set's loads right after its products:
-    // left to itself the compiler hoists all loads of an iteration to its
-    // top and then waits for every one of them
-    for (; i + 2 < nw; i += 2) {
-      vmma(f0, col_live, acc);
-      __builtin_amdgcn_sched_barrier(0);
-      vload(f0, rowp, actp, kof(i + 2), kh);
-      __builtin_amdgcn_sched_barrier(0);
-      vmma(f1, col_live, acc);
-      __builtin_amdgcn_sched_barrier(0);
-      vload(f1, rowp, actp, kof(i + 3), kh);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    vmma(f0, col_live, acc);
-    if (i + 1 < nw) vmma(f1, col_live, acc);
+  // staging: load j of this thread is chunk c of stage row r (r < 64: tile
+  // r / 32, tile row r % 32); chunks past the slice re-read its last chunk
+  const char* lrow[St::NLD];
+  int lds_off[St::NLD], lchunk[St::NLD];
+#pragma unroll
+  for (int j = 0; j < St::NLD; ++j) {
+    const int f = j * kGBlock + tid, r = f / St::CPR, c = f % St::CPR;
+    int n = tile_row[r / 32] + r % 32;
+    if (n_rows_w && n >= n_rows_w) n = n_rows_w - 1;
+    lrow[j] = (const char*)tile_w[r / 32] + (size_t)n * a.K * wbytes;
+    lds_off[j] = r * St::RS + c * 16;
+    lchunk[j] = c;
   }
+  const int kend = kbB * 32 * (int)wbytes - 16;  // last 16-byte chunk of the slice
+  auto gload = [&](uint4 (&R)[St::NLD], int st) {
+#pragma unroll
+    for (int j = 0; j < St::NLD; ++j) {
+      int off = (kbA + st * 8) * 32 * (int)wbytes + lchunk[j] * 16;
+      off = off < kend ? off : kend;
+      R[j] = ld_stream((const uint4*)(lrow[j] + off));
+    }
+  };
+  auto stage = [&](const uint4 (&R)[St::NLD]) {
+    __syncthreads();  // every wave is done with the previous stage
+#pragma unroll
+    for (int j = 0; j < St::NLD; ++j) *(uint4*)(smem + lds_off[j]) = R[j];
+    __syncthreads();
+  };
+  auto product = [&](int st) {
+    const int block = kbA + st * 8 + wid;
+    if (block < kbB) {
+      VFrag<WFMT, T> f;
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+        frag_lds<WFMT>(smem + (t * 32 + rl) * St::RS, wid, kh, f.wa[t], f.wb[t]);
+      const int b0 = block * 32;
+      f.ba = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + vk_lo<WFMT>(b0, kh)));
+      f.bb = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + vk_hi<WFMT>(b0, kh)));
+      vmma(f, col_live, acc);
+    }
+  };
+  if (nst > 0) {
+    // two stages in flight in registers; the scheduling barriers keep each
+    // set's refill right after it has gone to LDS
+    uint4 R0[St::NLD], R1[St::NLD];
+    gload(R0, 0);
+    gload(R1, 1);
+    int st = 0;
+    for (; st + 2 < nst; st += 2) {
+      stage(R0);
+      __builtin_amdgcn_sched_barrier(0);
+      gload(R0, st + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      product(st);
+      stage(R1);
+      __builtin_amdgcn_sched_barrier(0);
+      gload(R1, st + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      product(st + 1);
+    }
+    stage(R0);
+    product(st);
+    if (st + 1 < nst) {
+      stage(R1);
+      product(st + 1);
+    }
+  }
+  __syncthreads();  // the stage buffer becomes the partial-tile buffer
   // D layout: lane l, register v -> column j = l % 32,
   // row i = 8 * (v / 4) + 4 * (l / 32) + (v % 4).  The upper four waves
   // hand their tiles to the lower four, which then write the sums.
