@@ -66,27 +66,47 @@ struct VNormArgs {
   float eps;
 };
 
-// One workgroup per row r: h = x_r / sqrt(mean(x_r^2) + eps) * g, split.
-__global__ __launch_bounds__(kBlock) void k_vnorm(VNormArgs a) {
-  __shared__ float red[kWaves];
+// One workgroup of 1024 threads per row r: h = x_r / sqrt(mean(x_r^2) + eps)
+// * g, split.  Each thread keeps up to kNormVals of its elements in
+// registers between the two passes (all of them for d <= 8192).
+constexpr int kNormBlock = 1024;
+constexpr int kNormVals = 8;
+
+__global__ __launch_bounds__(kNormBlock) void k_vnorm(VNormArgs a) {
+  __shared__ float red[kNormBlock / AIO_WAVE];
   const int r = blockIdx.x, tid = threadIdx.x;
   const uint16_t* emb = a.embed ? a.embed + (size_t)a.st->token[r] * a.d : nullptr;
   const float* xr = a.x + (size_t)r * a.d;
+  auto val = [&](int e) { return emb ? bf16_to_f32(emb[e]) : xr[e]; };
+  float v[kNormVals];
   float ss = 0.f;
-  for (int e = tid; e < a.d; e += kBlock) {
-    const float v = emb ? bf16_to_f32(emb[e]) : xr[e];
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int i = 0; i < kNormVals; ++i) {
+    const int e = tid + i * kNormBlock;
+    v[i] = e < a.d ? val(e) : 0.f;
+    ss = fmaf(v[i], v[i], ss);
+  }
+  for (int e = tid + kNormVals * kNormBlock; e < a.d; e += kNormBlock) {
+    const float x = val(e);
+    ss = fmaf(x, x, ss);
   }
   ss = wave_sum(ss);
   if ((tid & (AIO_WAVE - 1)) == 0) red[tid / AIO_WAVE] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormBlock / AIO_WAVE; ++w) tot += red[w];
   const float inv = rsqrtf(tot / (float)a.d + a.eps);
-  for (int e = tid; e < a.d; e += kBlock) {
-    const float v = emb ? bf16_to_f32(emb[e]) : xr[e];
-    if (emb) a.x_copy[(size_t)r * a.d + e] = v;
-    store_split(a.act, a.lda, a.M, r, e, v * inv * bf16_to_f32(a.gain[e]));
+  auto out = [&](int e, float x) {
+    if (emb) a.x_copy[(size_t)r * a.d + e] = x;
+    store_split(a.act, a.lda, a.M, r, e, x * inv * bf16_to_f32(a.gain[e]));
+  };
+#pragma unroll
+  for (int i = 0; i < kNormVals; ++i) {
+    const int e = tid + i * kNormBlock;
+    if (e < a.d) out(e, v[i]);
   }
+  for (int e = tid + kNormVals * kNormBlock; e < a.d; e += kNormBlock) out(e, val(e));
 }
 
 // ------------------------------------------------------------- skinny GEMM
@@ -428,8 +448,8 @@ struct VAttnArgs {
 template <int HD>
 __global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
   constexpr int LPK = HD / 8, NG = kBlock / LPK;
-  __shared__ float sm_m[NG][kMaxRows], sm_l[NG][kMaxRows];
-  __shared__ float sm_o[NG][HD];
+  __shared__ float sm_m[kWaves][kMaxRows], sm_l[kWaves][kMaxRows];
+  __shared__ float sm_o[kWaves][kMaxRows][HD];
   const int tid = threadIdx.x, gi = tid / LPK, li = tid % LPK;
   const int s = blockIdx.x, h = blockIdx.y, G = a.H / a.Hkv, kvh = h / G;
   const int pos = a.st->pos, M = a.M;
@@ -489,40 +509,59 @@ __global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
       }
     }
   }
-  // combine the NG groups row by row (r is uniform across the block)
-  if (li == 0) {
+  // combine the groups: first the NG / kWaves groups of each wave with lane
+  // exchanges (every group of the wave ends with the wave's state), then the
+  // kWaves wave states through LDS, all rows at once
+#pragma unroll
+  for (int off = LPK; off < AIO_WAVE; off <<= 1) {
 #pragma unroll
     for (int r = 0; r < kMaxRows; ++r) {
-      sm_m[gi][r] = m[r];
-      sm_l[gi][r] = l[r];
+      if (r >= M) continue;
+      const float m2 = __shfl_xor(m[r], off, AIO_WAVE);
+      const float l2 = __shfl_xor(l[r], off, AIO_WAVE);
+      const float mx = fmaxf(m[r], m2);
+      const float c1 = m[r] == -INFINITY ? 0.f : exp2f(m[r] - mx);
+      const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - mx);
+      l[r] = l[r] * c1 + l2 * c2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[r][i] = o[r][i] * c1 + __shfl_xor(o[r][i], off, AIO_WAVE) * c2;
+      m[r] = mx;
     }
   }
+  const int wv = tid / AIO_WAVE;
+  if (tid % AIO_WAVE < LPK) {  // group 0 of each wave writes the wave's state
 #pragma unroll
-  for (int r = 0; r < kMaxRows; ++r) {
-    if (r >= M) continue;
-    __syncthreads();
+    for (int r = 0; r < kMaxRows; ++r) {
+      if (r >= M) continue;
+      if (li == 0) {
+        sm_m[wv][r] = m[r];
+        sm_l[wv][r] = l[r];
+      }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) sm_o[gi][li * 8 + i] = o[r][i];
-    __syncthreads();
-    for (int dim = tid; dim < HD; dim += kBlock) {
-      float Mx = -INFINITY;
-      for (int k = 0; k < NG; ++k) Mx = fmaxf(Mx, sm_m[k][r]);
-      float L = 0.f, O = 0.f;
-      if (Mx != -INFINITY) {
-        for (int k = 0; k < NG; ++k) {
-          const float mk = sm_m[k][r];
-          if (mk == -INFINITY) continue;
-          const float w = exp2f(mk - Mx);
-          L = fmaf(w, sm_l[k][r], L);
-          O = fmaf(w, sm_o[k][dim], O);
-        }
+      for (int i = 0; i < 8; ++i) sm_o[wv][r][li * 8 + i] = o[r][i];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < M * HD; e += kBlock) {
+    const int r = e / HD, dim = e % HD;
+    float Mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) Mx = fmaxf(Mx, sm_m[w][r]);
+    float L = 0.f, O = 0.f;
+    if (Mx != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float mk = sm_m[w][r];
+        const float wt = mk == -INFINITY ? 0.f : exp2f(mk - Mx);
+        L = fmaf(wt, sm_l[w][r], L);
+        O = fmaf(wt, sm_o[w][r][dim], O);
       }
-      const size_t slot = ((size_t)r * a.H + h) * a.S + s;
-      a.part_o[slot * HD + dim] = O;
-      if (dim == 0) {
-        a.part_ml[slot * 2] = Mx;
-        a.part_ml[slot * 2 + 1] = L;
-      }
+    }
+    const size_t slot = ((size_t)r * a.H + h) * a.S + s;
+    a.part_o[slot * HD + dim] = O;
+    if (dim == 0) {
+      a.part_ml[slot * 2] = Mx;
+      a.part_ml[slot * 2 + 1] = L;
     }
   }
 }
@@ -585,7 +624,7 @@ hipError_t launch_vnorm(const aio_model& m, const float* x, const uint16_t* embe
   n.M = M;
   n.st = m.state();
   n.eps = m.cfg.rms_eps;
-  hipLaunchKernelGGL(k_vnorm, dim3(M), dim3(kBlock), 0, m.stream, n);
+  hipLaunchKernelGGL(k_vnorm, dim3(M), dim3(kNormBlock), 0, m.stream, n);
   return hipGetLastError();
 }
 
