@@ -1066,10 +1066,9 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
   constexpr int NOUT = G * HD;            // outputs of a unit
   constexpr int R = kT / NOUT > 0 ? kT / NOUT : 1;  // threads per output
   static_assert(NGR % R == 0, "groups must split evenly");
-  float* sm_m = lds;                      // [NGR][G]
-  float* sm_l = lds + NGR * G;            // [NGR][G]
-  float* sm_o = lds + 2 * NGR * G;        // [NGR][G][HD]
-  float* sm_r = sm_o + NGR * G * HD;      // [R][NOUT] partial sums, then [R][G]
+  float* sm_m = lds;                      // [kW][G] wave states
+  float* sm_l = lds + NGR * G;            // [kW][G]
+  float* sm_o = lds + 2 * NGR * G;        // [kW][G][HD]
   const Thr T = thr();
   const int tid = T.tid, gi = tid / LPK, li = tid % LPK;
   const int wv = __builtin_amdgcn_readfirstlane(T.wave);
@@ -1151,50 +1150,57 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
                                   (v1.x >> 16) | (v1.y & 0xffff0000u), (v1.z >> 16) | (v1.w & 0xffff0000u));
       attend_key<HD, G>(kk, vv, gi == 0, q, o, m, l);
     }
-    // combine the NGR groups: R threads per output, NGR / R groups each
+    // combine the groups: the AIO_WAVE / LPK groups of each wave with lane
+    // exchanges (every group of the wave ends with the wave's state), then
+    // the kW wave states in LDS
 #pragma unroll
-    for (int gg = 0; gg < G; ++gg) {
-      if (li == 0) {
-        sm_m[gi * G + gg] = m[gg];
-        sm_l[gi * G + gg] = l[gg];
+    for (int off = LPK; off < AIO_WAVE; off <<= 1) {
+#pragma unroll
+      for (int gg = 0; gg < G; ++gg) {
+        const float m2 = __shfl_xor(m[gg], off, AIO_WAVE);
+        const float l2 = __shfl_xor(l[gg], off, AIO_WAVE);
+        const float mx = fmaxf(m[gg], m2);
+        const float c1 = m[gg] == -INFINITY ? 0.f : exp2f(m[gg] - mx);
+        const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - mx);
+        l[gg] = l[gg] * c1 + l2 * c2;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          o[gg][i] = o[gg][i] * c1 + __shfl_xor(o[gg][i], off, AIO_WAVE) * c2;
+        m[gg] = mx;
       }
+    }
+    if (T.lane < LPK) {  // group 0 of each wave
 #pragma unroll
-      for (int i = 0; i < 8; ++i) sm_o[(gi * G + gg) * HD + li * 8 + i] = o[gg][i];
+      for (int gg = 0; gg < G; ++gg) {
+        if (li == 0) {
+          sm_m[wv * G + gg] = m[gg];
+          sm_l[wv * G + gg] = l[gg];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sm_o[(wv * G + gg) * HD + li * 8 + i] = o[gg][i];
+      }
     }
     __syncthreads();
-    {
-      const int c = tid % NOUT, r = tid / NOUT;  // output c, part r
-      const int gg = c / HD, dim = c % HD;
+    if (tid < NOUT) {
+      const int gg = tid / HD, dim = tid % HD;
       float M = -INFINITY;
-      for (int kk = 0; kk < NGR; ++kk) M = fmaxf(M, sm_m[kk * G + gg]);
-      float Ls = 0.f, Os = 0.f;
-      if (r < R && M != -INFINITY) {
-        for (int kk = r * (NGR / R); kk < (r + 1) * (NGR / R); ++kk) {
-          const float mk = sm_m[kk * G + gg];
-          const float w = mk == -INFINITY ? 0.f : exp2f(mk - M);
-          Ls = fmaf(w, sm_l[kk * G + gg], Ls);
-          Os = fmaf(w, sm_o[(kk * G + gg) * HD + dim], Os);
-        }
-      }
-      __syncthreads();
-      if (r < R) {
-        sm_r[r * NOUT + c] = Os;
-        if (dim == 0) sm_r[R * NOUT + r * G + gg] = Ls;
-      }
-      __syncthreads();
-      if (tid < NOUT) {
-        float Ot = 0.f, Lt = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < R; ++kk) {
-          Ot += sm_r[kk * NOUT + c];
-          Lt += sm_r[R * NOUT + kk * G + gg];
+      for (int w = 0; w < kW; ++w) M = fmaxf(M, sm_m[w * G + gg]);
+      float Ot = 0.f, Lt = 0.f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < kW; ++w) {
+          const float mk = sm_m[w * G + gg];
+          const float wt = mk == -INFINITY ? 0.f : exp2f(mk - M);
+          Ot = fmaf(wt, sm_o[(w * G + gg) * HD + dim], Ot);
+          Lt = fmaf(wt, sm_l[w * G + gg], Lt);
         }
-        unsigned* slot = a.part + ((size_t)(u.g * G + gg) * S + u.s) * (HD + 2);
-        st_tag(slot + dim, Ot, vo);
-        if (dim == 0) {
-          st_tag(slot + HD, M, vo);
-          st_tag(slot + HD + 1, Lt, vo);
-        }
+      }
+      unsigned* slot = a.part + ((size_t)(u.g * G + gg) * S + u.s) * (HD + 2);
+      st_tag(slot + dim, Ot, vo);
+      if (dim == 0) {
+        st_tag(slot + HD, M, vo);
+        st_tag(slot + HD + 1, Lt, vo);
       }
     }
     __syncthreads();  // the LDS is reused by the next unit or the merge
