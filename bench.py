@@ -123,6 +123,34 @@ def pld_bench(dm, cfg, P, tau0, n, toks, logits) -> dict:
     return out
 
 
+def verify_bench(dm, cfg, P, tau0, n) -> int:
+    """Time n verify forwards (one warm-up first) of tau0 and the k drafts of
+    the planted 3-gram at position P; one JSON line."""
+    import torch
+    import synth
+    from paper_2604_09752_amd import traffic
+    _, drafts = synth.planted_drafts(cfg, synth.make_prompt(cfg), tau0)
+    k = len(drafts)
+    lg = dm.new_logits(k + 1)
+    dm.verify(tau0, drafts, P, lg)
+    dm.sync()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(dm.stream)
+    for _ in range(n):
+        dm.verify(tau0, drafts, P, lg)
+    ev1.record(dm.stream)
+    dm.sync()
+    ms = ev0.elapsed_time(ev1) / n
+    b = traffic.verify_bytes(cfg, P, k + 1)
+    status = dm.status()
+    dm.close()
+    print(json.dumps({"verify_rows": k + 1, "position": P, "runs": n, "ms_per_verify": round(ms, 4),
+                      "bytes_per_verify": int(b), "gbs": round(b / (ms * 1e-3) / 1e9, 1),
+                      "frac_of_peak": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "workload": workload_name(cfg)}), flush=True)
+    return 0 if status == 0 else 3
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +164,9 @@ def main() -> int:
     ap.add_argument("--pld", type=int, default=0, metavar="N",
                     help="also time N tokens of prompt-lookup decoding (3-gram drafts, k = 8), "
                          "with and without the greedy continuation planted in the history")
+    ap.add_argument("--verify-runs", type=int, default=0, metavar="N",
+                    help="instead of the decode bench, time N verify forwards of the token and "
+                         "the k drafts of the planted 3-gram at the prompt's end, and exit")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="instead of the decode bench, run a plain device-to-device copy of "
                          "BYTES (the reference kernel for HBM counter calibration) and exit")
@@ -161,6 +192,9 @@ def main() -> int:
         return 2
     cfg = synth.CONFIGS[args.config]
     P = cfg.prompt_len if not cfg.prefill_by_model else 0
+    if args.verify_runs > 0 and P == 0:
+        print("--verify-runs needs a workload with its prompt already in the cache", file=sys.stderr)
+        return 2
     t0 = time.time()
     w = synth.make_weights(cfg)
     kv_host = synth.make_kv(cfg)
@@ -168,6 +202,8 @@ def main() -> int:
     dm = DeviceModel(cfg, w, kv_init=kv_host)
     log("device model ready in %.1fs" % (time.time() - t0))
     tau0 = synth.first_token(cfg)
+    if args.verify_runs > 0:
+        return verify_bench(dm, cfg, P, tau0, args.verify_runs)
     chunk = min(cfg.n_steps, cfg.max_ctx - P)
     logits = dm.new_logits(1)[0]
     toks = torch.zeros(max(chunk, args.warmup, 1), dtype=torch.int32, device=dm.device)
