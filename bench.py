@@ -344,7 +344,7 @@ def main() -> int:
     status = dm.status()
     dm.close()
     if status != 0:
-        print("device status %d: a grid barrier timed out; the run is invalid" % status,
+        print("device status %d: a bounded wait of the step kernel gave up; the run is invalid" % status,
               file=sys.stderr)
         return 3
     print(json.dumps(result), flush=True)

@@ -201,27 +201,33 @@ int aio_profile_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev
 int aio_uses_step_kernel(const aio_model* m);
 
 /* Phase timing of one decode step of the persistent kernel: the same work as
- * aio_decode_step, with workgroup 0 recording the device clock as it leaves
- * each grid barrier.  phase_us (host, max_phases doubles) receives the time
- * between consecutive barrier exits, i.e. per layer: attention, O
- * projection, gate/up, down, next layer's QKV; *n_phases the count written.
- * Synchronises.  AIO_EUNSUPPORTED when the handle does not use that kernel. */
+ * aio_decode_step, with workgroup 0 recording the device clock as it
+ * publishes the outputs of each phase.  phase_us (host, max_phases doubles)
+ * receives the time between consecutive phases' outputs, i.e. per layer:
+ * attention, O projection, gate/up, down, next layer's QKV; *n_phases the
+ * count written.  Synchronises.  AIO_EUNSUPPORTED when the handle does not
+ * use that kernel. */
 int aio_trace_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, double* phase_us,
                    int32_t max_phases, int32_t* n_phases);
 
-/* Barrier timing of one step of the persistent kernel: every workgroup
- * records the device clock (100 MHz) when it arrives at and leaves each grid
- * barrier.  arrive and leave (host arrays of max_entries >= (5 L + 1) x
- * blocks) receive [barrier][workgroup] times (barrier 0 unused); n_barriers
- * and n_blocks the dimensions.  Allocates a device buffer and synchronises;
- * a profiling aid.  AIO_EUNSUPPORTED when the handle does not use that kernel. */
+/* Per-workgroup timing of one step of the persistent kernel, device clock
+ * (100 MHz).  Phase k = 5 l + 1 .. 5 l + 5 of layer l is QKV, attention, O,
+ * gate/up, down.  arrive[k][b] receives the time workgroup b published its
+ * outputs of phase k, leave[k][b] the time it had the inputs of phase k + 1
+ * (entry 0 unused).  With max_entries >= 4 (5 L + 1) x blocks, arrive also
+ * carries, after its first (5 L + 1) x blocks entries, [phase][workgroup][2]
+ * the start and end of each workgroup's weight loop (attention: the end of
+ * its splits and of its merge).  n_barriers and n_blocks receive the
+ * dimensions (5 L + 1 and blocks).  Allocates a device buffer and
+ * synchronises; a profiling aid.  AIO_EUNSUPPORTED when the handle does not
+ * use that kernel. */
 int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_dev,
                        uint64_t* arrive, uint64_t* leave, int32_t max_entries,
                        int32_t* n_barriers, int32_t* n_blocks);
 
 /* Synchronises the model's stream and reports the device-side status word:
- * 0, or 1 if a grid barrier of the persistent kernel gave up waiting (its
- * results are then invalid).  Synchronises. */
+ * 0, or 1 if a bounded wait of the persistent kernel for another
+ * workgroup's data gave up (its results are then invalid).  Synchronises. */
 int aio_device_status(aio_model* m, int32_t* status);
 
 /* ------------------------------------------ prompt-lookup decoding (host) */

@@ -72,7 +72,7 @@ class Pair:
         return self.orc.decode_step(self.kv_host, token, pos)
 
     def check_status(self):
-        assert self.gpu.status() == 0, "a grid barrier of the step kernel timed out"
+        assert self.gpu.status() == 0, "a bounded wait of the step kernel gave up"
 
     def close(self):
         self.check_status()
