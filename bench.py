@@ -123,6 +123,57 @@ def pld_bench(dm, cfg, P, tau0, n, toks, logits) -> dict:
     return out
 
 
+def dual_bench(r: int, rounds: int = 8) -> int:
+    """Both models of the paper's deployment resident in HBM at once (its
+    Section 5.3 measures 2.4 ms for switching between them): requests of r
+    greedy tokens (one device-resident loop and a synchronisation each),
+    first back to back on one model, then alternating between the 7B-class
+    and the 1B-class decoder.  The switch cost is what an alternating pair
+    of requests costs beyond one request of each on its own."""
+    import torch
+    import synth
+    from paper_2604_09752_amd.binding import DeviceModel
+    models = {}
+    for name in ("7b", "1b"):
+        cfg = synth.CONFIGS[name]
+        dm = DeviceModel(cfg, synth.make_weights(cfg), kv_init=synth.make_kv(cfg))
+        models[name] = (dm, cfg.prompt_len, synth.first_token(cfg), dm.new_logits(1)[0],
+                        torch.zeros(r, dtype=torch.int32, device=dm.device))
+        log("%s resident: %.1f GB of weights" % (name, sum(
+            t.numel() * t.element_size() for t in dm.dev.values()) / 1e9))
+
+    def request(name):
+        dm, P, tau0, lg, toks = models[name]
+        dm.greedy(tau0, P, r, toks, lg)
+        dm.sync()
+
+    for name in models:  # warm-up: graphs, kernels, caches
+        request(name)
+    alone = {}
+    for name in models:
+        t0 = time.perf_counter()
+        for _ in range(rounds):
+            request(name)
+        alone[name] = (time.perf_counter() - t0) / rounds
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        request("7b")
+        request("1b")
+    pair = (time.perf_counter() - t0) / rounds
+    out = {"request_tokens": r, "rounds": rounds,
+           "ms_per_request_7b": round(1e3 * alone["7b"], 3),
+           "ms_per_request_1b": round(1e3 * alone["1b"], 3),
+           "ms_per_alternating_pair": round(1e3 * pair, 3),
+           "switch_us": round(1e6 * (pair - alone["7b"] - alone["1b"]) / 2, 1),
+           "resident": {n: models[n][0].cfg.name for n in models}}
+    rc = 0
+    for dm, *_ in models.values():
+        rc = rc or (3 if dm.status() != 0 else 0)
+        dm.close()
+    print(json.dumps(out), flush=True)
+    return rc
+
+
 def verify_bench(dm, cfg, P, tau0, n) -> int:
     """Time n verify forwards (one warm-up first) of tau0 and the k drafts of
     the planted 3-gram at position P; one JSON line."""
@@ -167,6 +218,10 @@ def main() -> int:
     ap.add_argument("--verify-runs", type=int, default=0, metavar="N",
                     help="instead of the decode bench, time N verify forwards of the token and "
                          "the k drafts of the planted 3-gram at the prompt's end, and exit")
+    ap.add_argument("--dual", type=int, default=0, metavar="N",
+                    help="instead of the decode bench, keep the 1B-class and the 7B-class "
+                         "decoders resident together and time requests of N greedy tokens, back "
+                         "to back on one model and alternating between them; one JSON line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="instead of the decode bench, run a plain device-to-device copy of "
                          "BYTES (the reference kernel for HBM counter calibration) and exit")
@@ -190,6 +245,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.dual > 0:
+        return dual_bench(args.dual)
     cfg = synth.CONFIGS[args.config]
     P = cfg.prompt_len if not cfg.prefill_by_model else 0
     if args.verify_runs > 0 and P == 0:
