@@ -174,6 +174,46 @@ def dual_bench(r: int, rounds: int = 8) -> int:
     return rc
 
 
+def spec_bench(n: int, k: int = 4) -> int:
+    """The paper's DraftModel baseline (Section 4.2; about 4 TPS on its
+    system, Section 2.2): the 1B-class decoder drafts k tokens, the 7B-class
+    decoder verifies them in one forward.  Both hold the same synthetic 2K
+    context.  With unrelated random weights the target accepts almost
+    nothing, so this times the mechanism's cost per token against the 7B's
+    plain greedy loop."""
+    import torch
+    import synth
+    from paper_2604_09752_amd import binding
+    from paper_2604_09752_amd.binding import DeviceModel
+    ct, cd = synth.CONFIGS["7b"], synth.CONFIGS["1b"]
+    target = DeviceModel(ct, synth.make_weights(ct), kv_init=synth.make_kv(ct))
+    draft = DeviceModel(cd, synth.make_weights(cd), kv_init=synth.make_kv(cd))
+    P, tau0 = ct.prompt_len, synth.first_token(ct)
+    n = min(n, ct.max_ctx - P - k - 1)
+    lg = target.new_logits(1)[0]
+    toks = torch.zeros(n, dtype=torch.int32, device=target.device)
+    target.greedy(tau0, P, n, toks, lg)
+    target.sync()
+    t0 = time.perf_counter()
+    target.greedy(tau0, P, n, toks, lg)
+    target.sync()
+    t_greedy = time.perf_counter() - t0
+    ref = [int(x) for x in toks.cpu().numpy()]
+    binding.spec_generate(target, draft, P, tau0, min(n, 8), k)  # warm-up
+    t0 = time.perf_counter()
+    got, st = binding.spec_generate(target, draft, P, tau0, n, k)
+    dt = time.perf_counter() - t0
+    out = {"tokens": n, "k": k, "target": "7b", "draft": "1b",
+           "greedy_tokens_per_s": round(n / t_greedy, 2), "spec_tokens_per_s": round(n / dt, 2),
+           "identical_to_greedy": list(got) == ref,
+           "acceptance": round(st["accepted"] / max(1, st["drafted"]), 3), **st}
+    rc = 3 if (target.status() != 0 or draft.status() != 0) else 0
+    target.close()
+    draft.close()
+    print(json.dumps(out), flush=True)
+    return rc
+
+
 def verify_bench(dm, cfg, P, tau0, n) -> int:
     """Time n verify forwards (one warm-up first) of tau0 and the k drafts of
     the planted 3-gram at position P; one JSON line."""
@@ -222,6 +262,10 @@ def main() -> int:
                     help="instead of the decode bench, keep the 1B-class and the 7B-class "
                          "decoders resident together and time requests of N greedy tokens, back "
                          "to back on one model and alternating between them; one JSON line")
+    ap.add_argument("--spec", type=int, default=0, metavar="N",
+                    help="instead of the decode bench, time N tokens of the 7B-class decoder "
+                         "with drafts (k = 4) from the resident 1B-class decoder, beside the "
+                         "7B's plain greedy loop; one JSON line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="instead of the decode bench, run a plain device-to-device copy of "
                          "BYTES (the reference kernel for HBM counter calibration) and exit")
@@ -247,6 +291,8 @@ def main() -> int:
         return 2
     if args.dual > 0:
         return dual_bench(args.dual)
+    if args.spec > 0:
+        return spec_bench(args.spec)
     cfg = synth.CONFIGS[args.config]
     P = cfg.prompt_len if not cfg.prefill_by_model else 0
     if args.verify_runs > 0 and P == 0:

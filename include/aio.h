@@ -279,6 +279,40 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
                      int32_t n_new, int32_t ngram_max, int32_t ngram_min, int32_t k,
                      float* logits_dev, int32_t* argmax_dev, int32_t* out, aio_pld_stats* stats);
 
+/* ------------------------------------- draft-model speculative decoding */
+
+typedef struct aio_spec_stats {
+  int32_t rounds;      /* target forwards (verify calls plus single decode steps) */
+  int32_t drafted;     /* draft tokens scored by the target                       */
+  int32_t accepted;    /* draft tokens accepted                                   */
+  int32_t draft_steps; /* decode steps of the draft model                         */
+} aio_spec_stats;
+
+/* Greedy generation with a draft model (Section 4.2, the DraftModel
+ * baseline: the 1B model drafts for the 7B).  `target` and `draft` are two
+ * resident models with the same vocabulary whose caches both hold the
+ * sequence at positions 0..pos-1; `token` is consumed at pos.  Each round
+ * the draft decodes up to k tokens greedily from the current token, the
+ * target scores [token, drafts] in one aio_verify (one aio_decode_step when
+ * no draft is wanted), and the longest prefix of drafts in which every draft
+ * equals the target's argmax of the row before it is accepted; the target's
+ * argmax after it is the next token.  When every draft is accepted the
+ * draft model also consumes the last draft, so both caches hold the
+ * sequence; rows past the accepted prefix are overwritten later, never
+ * read.  out (host, n_new int32) receives the generated tokens, which equal
+ * those of plain greedy decoding of the target.  target_logits_dev (fp32
+ * [k+1][vocab]), draft_logits_dev (fp32 [vocab]), argmax_dev (int32 [k+1])
+ * and draft_tokens_dev (int32 [k]) are scratch, each 16-byte aligned (the
+ * int32 buffers 4-byte aligned); stats may be NULL.  Synchronises both
+ * models' streams twice per round.
+ * AIO_EINVAL: a null handle or buffer, or vocabularies that differ.
+ * AIO_ERANGE: token outside [0, vocab), pos < 0, n_new < 1, pos + n_new
+ * beyond either cache, k < 0 or k + 1 > the target's max_verify. */
+int aio_spec_generate(aio_model* target, aio_model* draft, int32_t pos, int32_t token,
+                      int32_t n_new, int32_t k, float* target_logits_dev,
+                      float* draft_logits_dev, int32_t* argmax_dev, int32_t* draft_tokens_dev,
+                      int32_t* out, aio_spec_stats* stats);
+
 #ifdef __cplusplus
 }
 #endif

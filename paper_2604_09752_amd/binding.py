@@ -44,6 +44,11 @@ class aio_pld_stats(ctypes.Structure):
                 ("drafted", ctypes.c_int32), ("accepted", ctypes.c_int32)]
 
 
+class aio_spec_stats(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_int32), ("drafted", ctypes.c_int32),
+                ("accepted", ctypes.c_int32), ("draft_steps", ctypes.c_int32)]
+
+
 class AioError(RuntimeError):
     def __init__(self, code: int, what: str):
         self.code = code
@@ -89,6 +94,8 @@ def lib():
         L.aio_pld_match.argtypes = [vp, i32, i32, i32, i32, vp, P(i32)]
         L.aio_pld_generate.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp,
                                        P(aio_pld_stats)]
+        L.aio_spec_generate.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp,
+                                        P(aio_spec_stats)]
         _lib = L
     return _lib
 
@@ -244,6 +251,30 @@ def aio_pld_generate(handle: int, history, pos: int, token: int, n_new: int, ngr
                                   _ptr(logits), _ptr(argmax_out), out.ctypes.data,
                                   ctypes.byref(st)), "aio_pld_generate")
     return out, {f: int(getattr(st, f)) for f, _ in aio_pld_stats._fields_}
+
+
+def aio_spec_generate(target: int, draft: int, pos: int, token: int, n_new: int, k: int,
+                      target_logits: torch.Tensor, draft_logits: torch.Tensor,
+                      argmax_out: torch.Tensor, draft_tokens: torch.Tensor):
+    """Greedy generation of the target with drafts from the draft model;
+    returns (tokens, stats)."""
+    out = np.zeros(int(n_new), dtype=np.int32)
+    st = aio_spec_stats()
+    _check(lib().aio_spec_generate(target, draft, int(pos), int(token), int(n_new), int(k),
+                                   _ptr(target_logits), _ptr(draft_logits), _ptr(argmax_out),
+                                   _ptr(draft_tokens), out.ctypes.data, ctypes.byref(st)),
+           "aio_spec_generate")
+    return out, {f: int(getattr(st, f)) for f, _ in aio_spec_stats._fields_}
+
+
+def spec_generate(target: "DeviceModel", draft: "DeviceModel", pos: int, token: int, n_new: int,
+                  k: int):
+    """Draft-model speculative generation over two resident models (synchronous)."""
+    tl = target.new_logits(k + 1)
+    dl = draft.new_logits(1)
+    am = torch.zeros(k + 1, dtype=torch.int32, device=target.device)
+    dt = torch.zeros(max(k, 1), dtype=torch.int32, device=draft.device)
+    return aio_spec_generate(target.handle, draft.handle, pos, token, n_new, k, tl, dl, am, dt)
 
 
 def aio_device_status(handle: int) -> int:

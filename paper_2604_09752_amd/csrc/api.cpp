@@ -481,6 +481,68 @@ int aio_device_status(aio_model* m, int32_t* status) {
 
 int aio_uses_step_kernel(const aio_model* m) { return m && m->use_mega ? 1 : 0; }
 
+// ------------------------------------------------ draft-model speculation
+
+int aio_spec_generate(aio_model* target, aio_model* draft, int32_t pos, int32_t token,
+                      int32_t n_new, int32_t k, float* target_logits_dev,
+                      float* draft_logits_dev, int32_t* argmax_dev, int32_t* draft_tokens_dev,
+                      int32_t* out, aio_spec_stats* stats) {
+  if (!target || !draft || !target_logits_dev || !draft_logits_dev || !argmax_dev ||
+      !draft_tokens_dev || !out)
+    return AIO_EINVAL;
+  if (!aligned16(target_logits_dev) || !aligned16(draft_logits_dev) ||
+      ((uintptr_t)argmax_dev & 3u) || ((uintptr_t)draft_tokens_dev & 3u))
+    return AIO_EINVAL;
+  const aio_config& ct = target->cfg;
+  const aio_config& cd = draft->cfg;
+  if (ct.vocab != cd.vocab) return AIO_EINVAL;
+  if (token < 0 || token >= ct.vocab || pos < 0 || n_new < 1 || k < 0 || k + 1 > ct.max_verify)
+    return AIO_ERANGE;
+  const int32_t ctx = std::min(ct.max_ctx, cd.max_ctx);
+  if ((int64_t)pos + n_new > ctx) return AIO_ERANGE;
+  aio_spec_stats st{};
+  int32_t d[AIO_MAX_VERIFY_ROWS], y[AIO_MAX_VERIFY_ROWS];
+  int32_t p = pos, t = token, made = 0;
+  hipError_t e;
+  while (made < n_new) {
+    const int kk = std::min(std::min(k, n_new - made - 1), ctx - 1 - p);
+    int rc;
+    if (kk > 0) {
+      // the draft consumes t, d1 .. d(kk-1) at p .. p+kk-1 and proposes d1 .. dkk
+      if ((rc = aio_decode_greedy(draft, t, p, kk, draft_tokens_dev, draft_logits_dev))) return rc;
+      e = hipMemcpyAsync(d, draft_tokens_dev, (size_t)kk * sizeof(int32_t), hipMemcpyDeviceToHost,
+                         draft->stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(draft->stream);
+      if (e != hipSuccess) return hip_fail(e);
+      st.draft_steps += kk;
+      rc = aio_verify(target, t, d, kk, p, target_logits_dev);
+    } else {
+      rc = aio_decode_step(target, t, p, target_logits_dev);
+    }
+    if (rc) return rc;
+    if ((rc = aio_argmax(target, target_logits_dev, kk + 1, ct.vocab, argmax_dev))) return rc;
+    e = hipMemcpyAsync(y, argmax_dev, (size_t)(kk + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
+                       target->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(target->stream);
+    if (e != hipSuccess) return hip_fail(e);
+    int a = 0;
+    while (a < kk && d[a] == y[a]) ++a;  // row a's argmax follows d[0..a)
+    st.rounds += 1;
+    st.drafted += kk;
+    st.accepted += a;
+    for (int i = 0; i <= a && made < n_new; ++i) out[made++] = y[i];
+    if (kk > 0 && a == kk && made < n_new) {
+      // every draft accepted: the draft model has not consumed the last one
+      if ((rc = aio_decode_step(draft, d[kk - 1], p + kk, draft_logits_dev))) return rc;
+      st.draft_steps += 1;
+    }
+    p += a + 1;
+    t = y[a];
+  }
+  if (stats) *stats = st;
+  return AIO_OK;
+}
+
 // ------------------------------------------------- prompt-lookup decoding
 
 int aio_pld_match(const int32_t* hist, int32_t n_hist, int32_t ngram_max, int32_t ngram_min,
