@@ -225,6 +225,18 @@ int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_d
                        uint64_t* arrive, uint64_t* leave, int32_t max_entries,
                        int32_t* n_barriers, int32_t* n_blocks);
 
+/* Calibrates the persistent kernel's split of the gate/up rows over its
+ * workgroups: runs `rounds` decode steps of `token` at `pos` (so it writes
+ * that cache row, like aio_decode_step) with every workgroup timing its
+ * gate/up loops, and after each moves every workgroup's share of rows
+ * halfway towards its measured streaming rate (CUs and XCDs stream at
+ * slightly different rates, steadily; an even split waits for the slowest).
+ * The split stays with the handle for all later steps; results are
+ * unchanged up to fp32 rounding order, which does not depend on the split.
+ * Synchronises.  AIO_ERANGE: rounds outside [1, 64] or a bad token or pos;
+ * AIO_EUNSUPPORTED when the handle does not use the persistent kernel. */
+int aio_tune_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, int32_t rounds);
+
 /* Synchronises the model's stream and reports the device-side status word:
  * 0, or 1 if a bounded wait of the persistent kernel for another
  * workgroup's data gave up (its results are then invalid).  Synchronises. */

@@ -94,6 +94,7 @@ def lib():
         L.aio_pld_match.argtypes = [vp, i32, i32, i32, i32, vp, P(i32)]
         L.aio_pld_generate.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp,
                                        P(aio_pld_stats)]
+        L.aio_tune_step.argtypes = [vp, i32, i32, vp, i32]
         L.aio_spec_generate.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                         P(aio_spec_stats)]
         _lib = L
@@ -371,6 +372,11 @@ class DeviceModel:
         am = torch.zeros(k + 1, dtype=torch.int32, device=self.device)
         return aio_pld_generate(self.handle, history, pos, token, n_new, ngram_max, ngram_min, k,
                                 logits, am)
+
+    def tune(self, token: int, pos: int, logits: torch.Tensor, rounds: int = 4) -> None:
+        """Calibrate the persistent kernel's gate/up split (aio_tune_step)."""
+        _check(lib().aio_tune_step(self.handle, int(token), int(pos), _ptr(logits), int(rounds)),
+               "aio_tune_step")
 
     def profile_step(self, token: int, pos: int, logits: torch.Tensor) -> np.ndarray:
         return aio_profile_step(self.handle, token, pos, logits, 6 * self.c.n_layers + 1)

@@ -71,6 +71,8 @@ struct aio_model {
   bool mega_coop;  // cooperative launch (default); plain launch when AIO_STEP_LAUNCH=plain
   int mega_blocks;
   MegaLayer* mega_layers;          // library-owned device table [n_layers]
+  int* gu_bounds_dev;              // library-owned [mega_blocks + 1] gate/up unit bounds
+  std::vector<int> gu_bounds;      // host copy
   unsigned long long* mega_trace;  // library-owned, allocated on first trace
   // profiling: when prof_ev is set, every launcher records one event after
   // each kernel it enqueues (aio_profile_step)

@@ -250,6 +250,16 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
     if (e == hipSuccess)
       e = hipMemcpy(m->mega_layers, tab.data(), tab.size() * sizeof(MegaLayer),
                     hipMemcpyHostToDevice);
+    if (e == hipSuccess) {
+      // gate/up rows start evenly split; aio_tune_step recalibrates them
+      const int nb = m->mega_blocks;
+      m->gu_bounds.resize((size_t)nb + 1);
+      for (int b = 0; b <= nb; ++b) m->gu_bounds[b] = (int)((long long)b * m->cfg.ffn_dim / nb);
+      e = hipMalloc((void**)&m->gu_bounds_dev, m->gu_bounds.size() * sizeof(int));
+      if (e == hipSuccess)
+        e = hipMemcpy(m->gu_bounds_dev, m->gu_bounds.data(), m->gu_bounds.size() * sizeof(int),
+                      hipMemcpyHostToDevice);
+    }
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
     if (e == hipSuccess)
       e = hipMemset(m->ws + m->lay.mega_xa, 0, m->lay.mega_end - m->lay.mega_xa);
@@ -257,6 +267,7 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
   if (e != hipSuccess) {
     if (m->rope) (void)hipFree(m->rope);
     if (m->mega_layers) (void)hipFree(m->mega_layers);
+    if (m->gu_bounds_dev) (void)hipFree(m->gu_bounds_dev);
     delete m;
     return hip_fail(e);
   }
@@ -273,6 +284,7 @@ void aio_model_free(aio_model* m) {
   if (m->greedy_exec) (void)hipGraphExecDestroy(m->greedy_exec);
   if (m->rope) (void)hipFree(m->rope);
   if (m->mega_layers) (void)hipFree(m->mega_layers);
+  if (m->gu_bounds_dev) (void)hipFree(m->gu_bounds_dev);
   if (m->mega_trace) (void)hipFree(m->mega_trace);
   delete m;
 }
@@ -464,6 +476,88 @@ int aio_trace_barriers(aio_model* m, int32_t token, int32_t pos, float* logits_d
   *n_barriers = nbar;
   *n_blocks = nblk;
   return AIO_OK;
+}
+
+// New gate/up split from measured loop times: each workgroup's share moves
+// halfway towards its streaming rate (units per unit of loop time), capped
+// at the LDS sizing; integer counts keep the sum.
+static void rebalance_gu(std::vector<int>& bounds, const std::vector<double>& loop_ticks,
+                         int total, int cap) {
+  const int nb = (int)bounds.size() - 1;
+  std::vector<double> units(nb), rate(nb);
+  double rsum = 0.0, usum = 0.0, tsum = 0.0;
+  for (int b = 0; b < nb; ++b) {
+    units[b] = bounds[b + 1] - bounds[b];
+    usum += units[b];
+    tsum += loop_ticks[b];
+  }
+  const double mean_rate = usum / std::max(tsum, 1.0);
+  for (int b = 0; b < nb; ++b) {
+    rate[b] = units[b] > 0 && loop_ticks[b] > 0 ? units[b] / loop_ticks[b] : mean_rate;
+    rsum += rate[b];
+  }
+  std::vector<double> want(nb);
+  double wsum = 0.0;
+  for (int b = 0; b < nb; ++b) {
+    const double target = total * rate[b] / rsum;
+    want[b] = std::min((double)cap, std::max(1.0, 0.5 * units[b] + 0.5 * target));
+    wsum += want[b];
+  }
+  std::vector<int> cnt(nb);
+  std::vector<std::pair<double, int>> frac;
+  int used = 0;
+  for (int b = 0; b < nb; ++b) {
+    const double x = want[b] * total / wsum;
+    cnt[b] = std::min(cap, (int)x);
+    used += cnt[b];
+    frac.push_back({x - (int)x, b});
+  }
+  std::sort(frac.begin(), frac.end(), [](const auto& p, const auto& q) { return p.first > q.first; });
+  for (int pass = 0; used < total && pass < 4; ++pass)
+    for (size_t i = 0; i < frac.size() && used < total; ++i)
+      if (cnt[frac[i].second] < cap) {
+        cnt[frac[i].second] += 1;
+        used += 1;
+      }
+  if (used != total) return;  // cannot happen while nb * cap >= total; keep the old split
+  bounds[0] = 0;
+  for (int b = 0; b < nb; ++b) bounds[b + 1] = bounds[b] + cnt[b];
+}
+
+int aio_tune_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, int32_t rounds) {
+  if (!m || !logits_dev || !aligned16(logits_dev)) return AIO_EINVAL;
+  int rc = aio_check_decode(&m->cfg, token, pos);
+  if (rc) return rc;
+  if (rounds < 1 || rounds > 64) return AIO_ERANGE;
+  if (!m->use_mega) return AIO_EUNSUPPORTED;
+  const int L = m->cfg.n_layers, nbar = 5 * L + 1, nblk = m->mega_blocks;
+  const size_t n = (size_t)nbar * (size_t)nblk;
+  const int cap = aio_step_kernel_gu_cap(m->cfg, nblk);
+  std::vector<unsigned long long> det(2 * n);
+  unsigned long long* dev = nullptr;  // arrive [n], leave [n], loop start/end [n][2]
+  hipError_t e = hipMalloc((void**)&dev, 4 * n * 8);
+  for (int r = 0; r < rounds && e == hipSuccess; ++r) {
+    e = hipMemsetAsync(dev, 0, 4 * n * 8, m->stream);
+    if (e == hipSuccess) e = aio_launch_set_state(*m, token, pos);
+    if (e == hipSuccess) e = aio_launch_step_kernel(*m, logits_dev, nullptr, nullptr, dev, dev + n);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e == hipSuccess) e = hipMemcpy(det.data(), dev + 2 * n, 2 * n * 8, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) break;
+    // gate/up loop time of each workgroup over the layers (phase 5 l + 4)
+    std::vector<double> ticks(nblk, 0.0);
+    for (int l = 0; l < L; ++l) {
+      const size_t k = (size_t)(5 * l + 4);
+      for (int b = 0; b < nblk; ++b) {
+        const unsigned long long t0 = det[(k * nblk + b) * 2], t1 = det[(k * nblk + b) * 2 + 1];
+        if (t1 > t0) ticks[b] += (double)(t1 - t0);
+      }
+    }
+    rebalance_gu(m->gu_bounds, ticks, m->cfg.ffn_dim, cap);
+    e = hipMemcpy(m->gu_bounds_dev, m->gu_bounds.data(), m->gu_bounds.size() * sizeof(int),
+                  hipMemcpyHostToDevice);
+  }
+  if (dev) (void)hipFree(dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
 }
 
 int aio_device_status(aio_model* m, int32_t* status) {

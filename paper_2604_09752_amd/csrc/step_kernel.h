@@ -56,12 +56,16 @@ struct MegaArgs {
   unsigned long long* bar_arrive;  // optional: [5 L + 1][blocks] publish time of phase k
   unsigned long long* bar_leave;   // optional: [5 L + 1][blocks] time the inputs of phase k + 1 were in
   unsigned long long* detail;      // optional: [5 L + 1][blocks][2] loop start and end of phase k
+  const int* gu_bounds;            // [blocks + 1] gate/up units of each workgroup (null: even split)
   int L, d, H, Hkv, hd, F, V, max_ctx, S;
   int red_words;   // floats of one LDS buffer of matrix-phase partials
   float eps, scale_log2;
 };
 
 bool aio_step_kernel_supports(const aio_config& c);
+// Most gate/up units (row pairs) one workgroup may own: the even share plus
+// an eighth (at least 2), which the LDS partial buffers are sized for.
+int aio_step_kernel_gu_cap(const aio_config& c, int blocks);
 int aio_step_kernel_vpl(const aio_config& c, int K);
 size_t aio_step_kernel_lds(const aio_config& c, int blocks);
 hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* tokens_out,

@@ -300,8 +300,15 @@ AIO_DEV GPhase make_phase(const MegaArgs& a, int layer) {
   const int nu = n_units<KIND>(a);
   P.nu = nu;
   const int b = blockIdx.x, nbk = gridDim.x;
-  P.u0 = (int)((long long)b * nu / nbk);
-  P.u1 = (int)((long long)(b + 1) * nu / nbk);
+  if (KIND == K_GU && a.gu_bounds) {
+    // calibrated split (aio_tune_step), read as wave-uniform scalars
+    typedef __attribute__((address_space(4))) const int cint;
+    P.u0 = ((cint*)a.gu_bounds)[b];
+    P.u1 = ((cint*)a.gu_bounds)[b + 1];
+  } else {
+    P.u0 = (int)((long long)b * nu / nbk);
+    P.u1 = (int)((long long)(b + 1) * nu / nbk);
+  }
   return P;
 }
 
@@ -1316,12 +1323,17 @@ bool aio_step_kernel_supports(const aio_config& c) {
   return true;
 }
 
+int aio_step_kernel_gu_cap(const aio_config& c, int blocks) {
+  const int even = (c.ffn_dim + blocks - 1) / blocks;
+  return even + std::max(2, even / 8);
+}
+
 // Floats of one buffer of matrix-phase partials: [units per workgroup][RPU][kW].
 static int red_words(const aio_config& c, int blocks) {
   auto red = [&](int units, int rpu) { return ((units + blocks - 1) / blocks) * rpu * kW; };
   int w = red((c.n_heads + 2 * c.n_kv_heads) * c.head_dim / 4, 4);
   w = std::max(w, red(c.d_model, 1));
-  w = std::max(w, red(c.ffn_dim, 2));
+  w = std::max(w, aio_step_kernel_gu_cap(c, blocks) * 2 * kW);
   w = std::max(w, red(c.vocab, 1));
   return (w + 63) & ~63;
 }
@@ -1364,6 +1376,7 @@ hipError_t aio_launch_step_kernel(const aio_model& m, float* logits, int32_t* to
   a.bar_arrive = bar_arrive;
   a.bar_leave = bar_leave;
   a.detail = bar_leave ? bar_leave + (size_t)(5 * c.n_layers + 1) * m.mega_blocks : nullptr;
+  a.gu_bounds = m.gu_bounds_dev;
   a.L = c.n_layers;
   a.d = c.d_model;
   a.H = c.n_heads;

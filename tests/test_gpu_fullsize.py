@@ -62,3 +62,18 @@ def test_int8_verify_planted_3gram():
         log("verify argmax gpu %s oracle %s" % (list(ids), [oracle.argmax(r) for r in ref]))
     finally:
         pair.close()
+
+
+def test_tuned_split_keeps_parity():
+    """After aio_tune_step moves gate/up rows between workgroups, decode still
+    matches the oracle (the 1B-class decoder, sampled teacher-forced steps)."""
+    cfg = synth.CONFIGS["1b"]
+    pair = Pair(cfg)
+    try:
+        tau0 = synth.first_token(cfg)
+        pair.gpu.tune(tau0, cfg.prompt_len, pair.logits[0], 4)
+        worst, agree, ties, _ = teacher_forced(pair, tau0, cfg.prompt_len, 3)
+        log("1b tuned: worst err/tol %.3e, argmax agree %d/3 (near ties %d)" % (worst, agree, ties))
+        assert agree + ties == 3
+    finally:
+        pair.close()
