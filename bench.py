@@ -174,6 +174,45 @@ def dual_bench(r: int, rounds: int = 8) -> int:
     return rc
 
 
+def probe_bench(n: int, reps: int = 5) -> int:
+    """The probe's front end (Section 3.2): the 1B-class decoder consumes an
+    n-token request (seeded random tokens standing in for the templated
+    prompt) from position 0 through the verify forward in chunks, then the
+    routing rule reads the logits of three seeded label tokens.  The paper
+    measures 11.8 ms for its probe's prefill (Section 5.3)."""
+    import torch
+    import synth
+    from paper_2604_09752_amd import binding
+    from paper_2604_09752_amd.binding import DeviceModel
+    cfg = synth.CONFIGS["1b"]
+    n = min(n, cfg.max_ctx)
+    dm = DeviceModel(cfg, synth.make_weights(cfg))
+    toks = synth.tokens(cfg.seed + 3, "probe_request", n, cfg.vocab)
+    labels = synth.tokens(cfg.seed + 3, "probe_labels", 3, cfg.vocab)
+    lg = dm.new_logits(cfg.max_verify)
+    dm.prefill(toks, 0, lg)
+    dm.sync()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(dm.stream)
+    for _ in range(reps):
+        dm.prefill(toks, 0, lg)
+    ev1.record(dm.stream)
+    dm.sync()
+    ms = ev0.elapsed_time(ev1) / reps
+    cat_logits = lg[0].cpu().numpy()[labels]
+    t0 = time.perf_counter()
+    small, h, cat = binding.aio_probe_route(cat_logits, 0, n)
+    route_us = (time.perf_counter() - t0) * 1e6
+    out = {"request_tokens": n, "prefill_ms": round(ms, 3),
+           "prefill_chunks": -(-n // cfg.max_verify), "entropy_nats": round(h, 4), "category": cat,
+           "route_to_small_model": small, "route_decision_us": round(route_us, 1),
+           "workload": workload_name(cfg)}
+    rc = 3 if dm.status() != 0 else 0
+    dm.close()
+    print(json.dumps(out), flush=True)
+    return rc
+
+
 def spec_bench(n: int, k: int = 4) -> int:
     """The paper's DraftModel baseline (Section 4.2; about 4 TPS on its
     system, Section 2.2): the 1B-class decoder drafts k tokens, the 7B-class
@@ -269,6 +308,9 @@ def main() -> int:
                     help="instead of the decode bench, time N tokens of the 7B-class decoder "
                          "with drafts (k = 4) from the resident 1B-class decoder, beside the "
                          "7B's plain greedy loop; one JSON line")
+    ap.add_argument("--probe", type=int, default=0, metavar="N",
+                    help="instead of the decode bench, time the 1B-class probe's prefill of an "
+                         "N-token request and its routing decision; one JSON line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="instead of the decode bench, run a plain device-to-device copy of "
                          "BYTES (the reference kernel for HBM counter calibration) and exit")
@@ -296,6 +338,8 @@ def main() -> int:
         return dual_bench(args.dual)
     if args.spec > 0:
         return spec_bench(args.spec)
+    if args.probe > 0:
+        return probe_bench(args.probe)
     cfg = synth.CONFIGS[args.config]
     P = cfg.prompt_len if not cfg.prefill_by_model else 0
     if args.verify_runs > 0 and P == 0:

@@ -291,6 +291,32 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
                      int32_t n_new, int32_t ngram_max, int32_t ngram_min, int32_t k,
                      float* logits_dev, int32_t* argmax_dev, int32_t* out, aio_pld_stats* stats);
 
+/* -------------------------------------------- the probe's front end (host) */
+
+/* Consumes tokens[0..n) (host) at positions pos .. pos+n-1 through the verify
+ * forward, in chunks of max_verify rows (Section 3.2, "Probe-Based
+ * Request-Level Intent Sensing": the probe runs one forward over the
+ * templated request).  Writes every token's K/V; logits_dev (fp32
+ * [max_verify][vocab], 16-byte aligned) is scratch, and on return its row 0
+ * holds the logits after the last token.  Asynchronous like aio_verify.
+ * AIO_ERANGE: n < 1, pos < 0, pos + n > max_ctx or a token outside
+ * [0, vocab); AIO_EINVAL: a null pointer. */
+int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev);
+
+/* The probe's routing decision (Section 3.2 and Section 3.3, "Dynamic
+ * Policy Routing and Execution"), pure host: the categories' scores are the
+ * probe's logits of the n_categories label tokens (host array).  The
+ * category is their argmax (lowest index on ties) and H(X) the Shannon
+ * entropy, in nats, of their softmax.  The request goes to the small model
+ * (return 1) when the category is `code_category`, ctx_len <= ctx_limit and
+ * H(X) <= tau; otherwise to the large one (return 0).  *entropy and
+ * *category receive H(X) and the category when not NULL.  Negative error
+ * code (AIO_EINVAL: null logits; AIO_ERANGE: n_categories < 1 or
+ * code_category outside [0, n_categories)) on bad arguments. */
+int aio_probe_route(const float* category_logits, int32_t n_categories, int32_t code_category,
+                    int32_t ctx_len, int32_t ctx_limit, float tau, float* entropy,
+                    int32_t* category);
+
 /* ------------------------------------- draft-model speculative decoding */
 
 typedef struct aio_spec_stats {

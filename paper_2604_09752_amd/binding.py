@@ -95,6 +95,9 @@ def lib():
         L.aio_pld_generate.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp,
                                        P(aio_pld_stats)]
         L.aio_tune_step.argtypes = [vp, i32, i32, vp, i32]
+        L.aio_prefill.argtypes = [vp, vp, i32, i32, vp]
+        L.aio_probe_route.argtypes = [vp, i32, i32, i32, i32, ctypes.c_float,
+                                      P(ctypes.c_float), P(i32)]
         L.aio_spec_generate.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                         P(aio_spec_stats)]
         _lib = L
@@ -278,6 +281,18 @@ def spec_generate(target: "DeviceModel", draft: "DeviceModel", pos: int, token: 
     return aio_spec_generate(target.handle, draft.handle, pos, token, n_new, k, tl, dl, am, dt)
 
 
+def aio_probe_route(category_logits, code_category: int, ctx_len: int, ctx_limit: int = 2048,
+                    tau: float = 0.45):
+    """(route to the small model?, entropy in nats, category) of the probe."""
+    x = np.ascontiguousarray(category_logits, dtype=np.float32)
+    h, cat = ctypes.c_float(0.0), ctypes.c_int32(-1)
+    rc = lib().aio_probe_route(x.ctypes.data, int(x.size), int(code_category), int(ctx_len),
+                               int(ctx_limit), float(tau), ctypes.byref(h), ctypes.byref(cat))
+    if rc < 0:
+        raise AioError(rc, "aio_probe_route")
+    return bool(rc), float(h.value), int(cat.value)
+
+
 def aio_device_status(handle: int) -> int:
     st = ctypes.c_int32(0)
     _check(lib().aio_device_status(handle, ctypes.byref(st)), "aio_device_status")
@@ -372,6 +387,13 @@ class DeviceModel:
         am = torch.zeros(k + 1, dtype=torch.int32, device=self.device)
         return aio_pld_generate(self.handle, history, pos, token, n_new, ngram_max, ngram_min, k,
                                 logits, am)
+
+    def prefill(self, tokens, pos: int, logits: torch.Tensor) -> None:
+        """Consume tokens at pos.. through the verify forward; row 0 of logits
+        (max_verify rows) ends with the last token's logits."""
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        _check(lib().aio_prefill(self.handle, t.ctypes.data, int(t.size), int(pos), _ptr(logits)),
+               "aio_prefill")
 
     def tune(self, token: int, pos: int, logits: torch.Tensor, rounds: int = 4) -> None:
         """Calibrate the persistent kernel's gate/up split (aio_tune_step)."""

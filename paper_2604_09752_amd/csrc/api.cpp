@@ -575,6 +575,52 @@ int aio_device_status(aio_model* m, int32_t* status) {
 
 int aio_uses_step_kernel(const aio_model* m) { return m && m->use_mega ? 1 : 0; }
 
+// ---------------------------------------------------- the probe's front end
+
+int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev) {
+  if (!m || !tokens || !logits_dev || !aligned16(logits_dev)) return AIO_EINVAL;
+  const aio_config& c = m->cfg;
+  if (n < 1 || pos < 0 || (int64_t)pos + n > c.max_ctx) return AIO_ERANGE;
+  for (int32_t i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c.vocab) return AIO_ERANGE;
+  int32_t done = 0, rows = 0;
+  while (done < n) {
+    rows = std::min(n - done, c.max_verify);
+    const int rc = aio_verify(m, tokens[done], tokens + done + 1, rows - 1, pos + done, logits_dev);
+    if (rc) return rc;
+    done += rows;
+  }
+  if (rows > 1) {  // the last row's logits to row 0
+    const hipError_t e = hipMemcpyAsync(logits_dev, logits_dev + (size_t)(rows - 1) * c.vocab,
+                                        (size_t)c.vocab * sizeof(float), hipMemcpyDeviceToDevice,
+                                        m->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return AIO_OK;
+}
+
+int aio_probe_route(const float* category_logits, int32_t n_categories, int32_t code_category,
+                    int32_t ctx_len, int32_t ctx_limit, float tau, float* entropy,
+                    int32_t* category) {
+  if (!category_logits) return AIO_EINVAL;
+  if (n_categories < 1 || code_category < 0 || code_category >= n_categories) return AIO_ERANGE;
+  int best = 0;
+  for (int i = 1; i < n_categories; ++i)
+    if (category_logits[i] > category_logits[best]) best = i;
+  // softmax entropy in double: H = log(Z) - sum p_i (x_i - max), Z = sum e^(x_i - max)
+  const double mx = category_logits[best];
+  double z = 0.0, ez = 0.0;
+  for (int i = 0; i < n_categories; ++i) {
+    const double d = (double)category_logits[i] - mx, w = exp(d);
+    z += w;
+    ez += w * d;
+  }
+  const float h = (float)(log(z) - ez / z);  // the value reported is the value compared
+  if (entropy) *entropy = h;
+  if (category) *category = best;
+  return best == code_category && ctx_len <= ctx_limit && h <= tau ? 1 : 0;
+}
+
 // ------------------------------------------------ draft-model speculation
 
 int aio_spec_generate(aio_model* target, aio_model* draft, int32_t pos, int32_t token,
