@@ -33,8 +33,8 @@ int env_int(const char* name, int dflt) {
 // Split-KV partitions per head for the per-operation and verify attention:
 // (split, kv head) workgroups to cover the 256 CUs once for caches of up to
 // 8K positions (a workgroup's fixed cost then outweighs its keys; measured
-// on the 7B verify: 8 splits 5.65 ms, 16 splits 5.84 ms at 2K) and about
-// twice beyond (16 splits 12.1 ms, 8 splits 14.7 ms at 32K), but no split
+// on the 7B verify at 2K: 4, 8, 16 splits 5.48, 5.24, 5.85 ms) and about
+// twice beyond (at 32K: 16 splits 11.3 ms, 32 splits 12.4 ms), but no split
 // shorter than 64 keys at full context.
 int choose_splits(const aio_config& c) {
   int s = env_int("AIO_SPLITS", 0);

@@ -443,14 +443,23 @@ struct VAttnArgs {
   float scale_log2;
 };
 
+// The verify rows are cut into groups of kAttnRG; each row group has its own
+// kAttnWaves waves over the same keys, so a wave holds the state of kAttnRG
+// rows only (two waves per SIMD instead of one).
+constexpr int kAttnRG = 5;
+constexpr int kAttnRowGroups = (kMaxRows + kAttnRG - 1) / kAttnRG;
+constexpr int kAttnWaves = 4;
+constexpr int kAttnBlock = kAttnRowGroups * kAttnWaves * AIO_WAVE;
+
 // One workgroup per (split s, query head h).  Keys [0, pos + M - 1] are cut
 // into S splits; row r only takes keys j <= pos + r.
 template <int HD>
-__global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
-  constexpr int LPK = HD / 8, NG = kBlock / LPK;
-  __shared__ float sm_m[kWaves][kMaxRows], sm_l[kWaves][kMaxRows];
-  __shared__ float sm_o[kWaves][kMaxRows][HD];
-  const int tid = threadIdx.x, gi = tid / LPK, li = tid % LPK;
+__global__ __launch_bounds__(kAttnBlock) void k_vattn(VAttnArgs a) {
+  constexpr int LPK = HD / 8, RGT = kAttnWaves * AIO_WAVE, NG = RGT / LPK;
+  __shared__ float sm_m[kAttnWaves][kMaxRows], sm_l[kAttnWaves][kMaxRows];
+  __shared__ float sm_o[kAttnWaves][kMaxRows][HD];
+  const int tid = threadIdx.x, rt = tid % RGT, r0 = (tid / RGT) * kAttnRG;
+  const int gi = rt / LPK, li = rt % LPK;
   const int s = blockIdx.x, h = blockIdx.y, G = a.H / a.Hkv, kvh = h / G;
   const int pos = a.st->pos, M = a.M;
   const int n_keys = pos + M;
@@ -458,65 +467,88 @@ __global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
   const int j0 = s * chunk, j1 = min(n_keys, j0 + chunk);
   const size_t Hd = (size_t)a.H * HD;
 
-  float q[kMaxRows][8], o[kMaxRows][8], m[kMaxRows], l[kMaxRows];
+  float q[kAttnRG][8], o[kAttnRG][8], m[kAttnRG], l[kAttnRG];
 #pragma unroll
-  for (int r = 0; r < kMaxRows; ++r) {
+  for (int r = 0; r < kAttnRG; ++r) {
     m[r] = -INFINITY;
     l[r] = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      q[r][i] = r < M ? a.q[r * Hd + (size_t)h * HD + li * 8 + i] * a.scale_log2 : 0.f;
+      q[r][i] = r0 + r < M ? a.q[(r0 + r) * Hd + (size_t)h * HD + li * 8 + i] * a.scale_log2 : 0.f;
       o[r][i] = 0.f;
     }
   }
   const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD + li * 8;
   const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD + li * 8;
-  // four keys per group are requested before any is used (a key past the
-  // split reads the split's first row and is masked), then each is scored
-  // against every row with a DPP sum over the group's lanes
-  for (int j = j0 + gi; j < j1; j += 4 * NG) {
-    uint4 kk[4], vv[4];
-    bool valid[4];
+  // a group takes four keys at a time (a key past the split reads the
+  // split's first row and is masked); the next four are requested before the
+  // current ones are used
+  auto fetch = [&](int j, uint4 (&kk)[4], uint4 (&vv)[4]) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int jj = j + u * NG;
-      valid[u] = jj < j1;
-      const size_t off = (size_t)(valid[u] ? jj : j0) * HD;
+      const size_t off = (size_t)(jj < j1 ? jj : j0) * HD;
       kk[u] = *(const uint4*)(kbase + off);
       vv[u] = *(const uint4*)(vbase + off);
     }
+  };
+  uint4 kk[4], vv[4];
+  int j = j0 + gi;
+  const bool rows_here = r0 < M;
+  if (rows_here && j < j1) fetch(j, kk, vv);
+  for (; rows_here && j < j1; j += 4 * NG) {
+    uint4 nk[4], nv[4];
+    if (j + 4 * NG < j1) fetch(j + 4 * NG, nk, nv);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int jj = j + u * NG;
-      const float vf[8] = {bf16_lo(vv[u].x), bf16_hi(vv[u].x), bf16_lo(vv[u].y), bf16_hi(vv[u].y),
-                           bf16_lo(vv[u].z), bf16_hi(vv[u].z), bf16_lo(vv[u].w), bf16_hi(vv[u].w)};
+    for (int r = 0; r < kAttnRG; ++r) {
+      if (r0 + r < M) {
+        // the four scores, each summed over the group's lanes
+        float sc[4];
+        float mn = m[r];
 #pragma unroll
-      for (int r = 0; r < kMaxRows; ++r) {
-        if (r < M) {
-          float sc = dot8_bf16(kk[u], make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
-                               make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f);
-          sc = group_sum_dpp<LPK>(sc);
-          // causal: row r sees keys [0, pos + r]; masked keys leave the state
-          const bool take = valid[u] && jj <= pos + r;
-          const float mn = take ? fmaxf(m[r], sc) : m[r];
-          const float c = take ? exp2f(m[r] - mn) : 1.f;
-          const float p = take ? exp2f(sc - mn) : 0.f;
-          l[r] = l[r] * c + p;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) o[r][i] = fmaf(p, vf[i], o[r][i] * c);
-          m[r] = mn;
+        for (int u = 0; u < 4; ++u) {
+          const int jj = j + u * NG;
+          sc[u] = group_sum_dpp<LPK>(
+              dot8_bf16(kk[u], make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
+                        make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f));
+          // causal: row r0 + r sees keys [0, pos + r0 + r]
+          if (!(jj < j1 && jj <= pos + r0 + r)) sc[u] = -INFINITY;
+          mn = fmaxf(mn, sc[u]);
         }
+        // one rescale of the state for the four keys
+        const float c = mn == -INFINITY ? 1.f : exp2f(m[r] - mn);
+        float p[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) p[u] = sc[u] == -INFINITY ? 0.f : exp2f(sc[u] - mn);
+        l[r] = l[r] * c + ((p[0] + p[1]) + (p[2] + p[3]));
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[r][i] *= c;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t w[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            o[r][2 * i] = fmaf(p[u], bf16_lo(w[i]), o[r][2 * i]);
+            o[r][2 * i + 1] = fmaf(p[u], bf16_hi(w[i]), o[r][2 * i + 1]);
+          }
+        }
+        m[r] = mn;
       }
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      kk[u] = nk[u];
+      vv[u] = nv[u];
+    }
   }
-  // combine the groups: first the NG / kWaves groups of each wave with lane
-  // exchanges (every group of the wave ends with the wave's state), then the
-  // kWaves wave states through LDS, all rows at once
+  // combine the groups: first the NG / kAttnWaves groups of each wave with
+  // lane exchanges (every group of the wave ends with the wave's state), then
+  // the kAttnWaves wave states of each row group through LDS
 #pragma unroll
   for (int off = LPK; off < AIO_WAVE; off <<= 1) {
 #pragma unroll
-    for (int r = 0; r < kMaxRows; ++r) {
-      if (r >= M) continue;
+    for (int r = 0; r < kAttnRG; ++r) {
+      if (r0 + r >= M) continue;
       const float m2 = __shfl_xor(m[r], off, AIO_WAVE);
       const float l2 = __shfl_xor(l[r], off, AIO_WAVE);
       const float mx = fmaxf(m[r], m2);
@@ -528,29 +560,30 @@ __global__ __launch_bounds__(kBlock) void k_vattn(VAttnArgs a) {
       m[r] = mx;
     }
   }
-  const int wv = tid / AIO_WAVE;
-  if (tid % AIO_WAVE < LPK) {  // group 0 of each wave writes the wave's state
+  const int wv = rt / AIO_WAVE;
+  if (rt % AIO_WAVE < LPK) {  // group 0 of each wave writes the wave's state
 #pragma unroll
-    for (int r = 0; r < kMaxRows; ++r) {
-      if (r >= M) continue;
+    for (int r = 0; r < kAttnRG; ++r) {
+      const int R = r0 + r;
+      if (R >= M) continue;
       if (li == 0) {
-        sm_m[wv][r] = m[r];
-        sm_l[wv][r] = l[r];
+        sm_m[wv][R] = m[r];
+        sm_l[wv][R] = l[r];
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) sm_o[wv][r][li * 8 + i] = o[r][i];
+      for (int i = 0; i < 8; ++i) sm_o[wv][R][li * 8 + i] = o[r][i];
     }
   }
   __syncthreads();
-  for (int e = tid; e < M * HD; e += kBlock) {
+  for (int e = tid; e < M * HD; e += kAttnBlock) {
     const int r = e / HD, dim = e % HD;
     float Mx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) Mx = fmaxf(Mx, sm_m[w][r]);
+    for (int w = 0; w < kAttnWaves; ++w) Mx = fmaxf(Mx, sm_m[w][r]);
     float L = 0.f, O = 0.f;
     if (Mx != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
+      for (int w = 0; w < kAttnWaves; ++w) {
         const float mk = sm_m[w][r];
         const float wt = mk == -INFINITY ? 0.f : exp2f(mk - Mx);
         L = fmaf(wt, sm_l[w][r], L);
@@ -665,9 +698,9 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx; t.S = m.lay.splits; t.M = M;
     t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
     if (hd == 128)
-      hipLaunchKernelGGL(k_vattn<128>, dim3(t.S, H), dim3(kBlock), 0, m.stream, t);
+      hipLaunchKernelGGL(k_vattn<128>, dim3(t.S, H), dim3(kAttnBlock), 0, m.stream, t);
     else
-      hipLaunchKernelGGL(k_vattn<64>, dim3(t.S, H), dim3(kBlock), 0, m.stream, t);
+      hipLaunchKernelGGL(k_vattn<64>, dim3(t.S, H), dim3(kAttnBlock), 0, m.stream, t);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     VMergeArgs mg{t.part_o, t.part_ml, actB, ka, t.S, hd, H, M};
     hipLaunchKernelGGL(k_vmerge, dim3(H, M), dim3(128), 0, m.stream, mg);
