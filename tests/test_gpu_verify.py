@@ -40,7 +40,7 @@ def test_verify_equals_sequential_decode(name):
     try:
         P = cfg.prompt_len
         rng = np.random.default_rng(11)
-        for k in (0, 2, 8, 9):
+        for k in (0, 2, 4, 5, 8, 9):
             token = int(rng.integers(0, cfg.vocab))
             drafts = rng.integers(0, cfg.vocab, k).astype(np.int32)
             kv_before = pair.kv_host.copy()
