@@ -443,18 +443,26 @@ struct VAttnArgs {
   float scale_log2;
 };
 
-// The verify rows are cut into groups of kAttnRG; each row group has its own
-// kAttnWaves waves over the same keys, so a wave holds the state of kAttnRG
-// rows only (two waves per SIMD instead of one).
-constexpr int kAttnRG = 5;
-constexpr int kAttnRowGroups = (kMaxRows + kAttnRG - 1) / kAttnRG;
+// The verify rows are cut into groups of RG; each row group has its own
+// kAttnWaves waves over the same keys, so a wave holds the state of RG rows
+// only.  A lane group takes KB keys at a time, with the next KB requested
+// before the current ones are scored when PF is set.  Two shapes:
+//   RG 3, KB 2     four row groups, 122 VGPRs, four waves per SIMD: best
+//                  where the keys are few (2K: 5.12 against 5.20 ms per 7B
+//                  verify);
+//   RG 5, KB 4, PF two row groups, 226 VGPRs: each key is read by fewer
+//                  row groups, which wins where the keys are many (32K:
+//                  11.1 against 11.7 ms).
 constexpr int kAttnWaves = 4;
-constexpr int kAttnBlock = kAttnRowGroups * kAttnWaves * AIO_WAVE;
+template <int RG>
+constexpr int attn_block() { return (kMaxRows + RG - 1) / RG * kAttnWaves * AIO_WAVE; }
+static_assert(attn_block<3>() <= 1024, "verify attention workgroup too large");
 
 // One workgroup per (split s, query head h).  Keys [0, pos + M - 1] are cut
 // into S splits; row r only takes keys j <= pos + r.
-template <int HD>
-__global__ __launch_bounds__(kAttnBlock) void k_vattn(VAttnArgs a) {
+template <int HD, int RG, int KB, bool PF>
+__global__ __launch_bounds__(attn_block<RG>()) void k_vattn(VAttnArgs a) {
+  constexpr int kAttnRG = RG, kAttnBlock = attn_block<RG>();
   constexpr int LPK = HD / 8, RGT = kAttnWaves * AIO_WAVE, NG = RGT / LPK;
   __shared__ float sm_m[kAttnWaves][kMaxRows], sm_l[kAttnWaves][kMaxRows];
   __shared__ float sm_o[kAttnWaves][kMaxRows][HD];
@@ -480,33 +488,36 @@ __global__ __launch_bounds__(kAttnBlock) void k_vattn(VAttnArgs a) {
   }
   const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD + li * 8;
   const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD + li * 8;
-  // a group takes four keys at a time (a key past the split reads the
-  // split's first row and is masked); the next four are requested before the
-  // current ones are used
-  auto fetch = [&](int j, uint4 (&kk)[4], uint4 (&vv)[4]) {
+  // a group requests its KB keys before scoring any (a key past the split
+  // reads the split's first row and is masked)
+  auto fetch = [&](int j, uint4 (&kk)[KB], uint4 (&vv)[KB]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < KB; ++u) {
       const int jj = j + u * NG;
       const size_t off = (size_t)(jj < j1 ? jj : j0) * HD;
       kk[u] = *(const uint4*)(kbase + off);
       vv[u] = *(const uint4*)(vbase + off);
     }
   };
-  uint4 kk[4], vv[4];
+  uint4 kk[KB], vv[KB];
   int j = j0 + gi;
   const bool rows_here = r0 < M;
-  if (rows_here && j < j1) fetch(j, kk, vv);
-  for (; rows_here && j < j1; j += 4 * NG) {
-    uint4 nk[4], nv[4];
-    if (j + 4 * NG < j1) fetch(j + 4 * NG, nk, nv);
+  if (PF && rows_here && j < j1) fetch(j, kk, vv);
+  for (; rows_here && j < j1; j += KB * NG) {
+    uint4 nk[KB], nv[KB];
+    if constexpr (PF) {
+      if (j + KB * NG < j1) fetch(j + KB * NG, nk, nv);
+    } else {
+      fetch(j, kk, vv);
+    }
 #pragma unroll
     for (int r = 0; r < kAttnRG; ++r) {
       if (r0 + r < M) {
-        // the four scores, each summed over the group's lanes
-        float sc[4];
+        // the scores, each summed over the group's lanes
+        float sc[KB];
         float mn = m[r];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < KB; ++u) {
           const int jj = j + u * NG;
           sc[u] = group_sum_dpp<LPK>(
               dot8_bf16(kk[u], make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
@@ -515,16 +526,20 @@ __global__ __launch_bounds__(kAttnBlock) void k_vattn(VAttnArgs a) {
           if (!(jj < j1 && jj <= pos + r0 + r)) sc[u] = -INFINITY;
           mn = fmaxf(mn, sc[u]);
         }
-        // one rescale of the state for the four keys
+        // one rescale of the state per batch of keys
         const float c = mn == -INFINITY ? 1.f : exp2f(m[r] - mn);
-        float p[4];
+        float p[KB];
+        float ps = 0.f;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) p[u] = sc[u] == -INFINITY ? 0.f : exp2f(sc[u] - mn);
-        l[r] = l[r] * c + ((p[0] + p[1]) + (p[2] + p[3]));
+        for (int u = 0; u < KB; ++u) {
+          p[u] = sc[u] == -INFINITY ? 0.f : exp2f(sc[u] - mn);
+          ps += p[u];
+        }
+        l[r] = l[r] * c + ps;
 #pragma unroll
         for (int i = 0; i < 8; ++i) o[r][i] *= c;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < KB; ++u) {
           const uint32_t w[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -535,10 +550,12 @@ __global__ __launch_bounds__(kAttnBlock) void k_vattn(VAttnArgs a) {
         m[r] = mn;
       }
     }
+    if constexpr (PF) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      kk[u] = nk[u];
-      vv[u] = nv[u];
+      for (int u = 0; u < KB; ++u) {
+        kk[u] = nk[u];
+        vv[u] = nv[u];
+      }
     }
   }
   // combine the groups: first the NG / kAttnWaves groups of each wave with
@@ -697,10 +714,20 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     t.st = m.state();
     t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx; t.S = m.lay.splits; t.M = M;
     t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
-    if (hd == 128)
-      hipLaunchKernelGGL(k_vattn<128>, dim3(t.S, H), dim3(kAttnBlock), 0, m.stream, t);
+    // row groups of 3 up to 8K positions, of 5 beyond
+    const bool few = c.max_ctx <= 8192;
+    if (hd == 128 && few)
+      hipLaunchKernelGGL((k_vattn<128, 3, 2, false>), dim3(t.S, H), dim3(attn_block<3>()), 0,
+                         m.stream, t);
+    else if (hd == 128)
+      hipLaunchKernelGGL((k_vattn<128, 5, 4, true>), dim3(t.S, H), dim3(attn_block<5>()), 0,
+                         m.stream, t);
+    else if (few)
+      hipLaunchKernelGGL((k_vattn<64, 3, 2, false>), dim3(t.S, H), dim3(attn_block<3>()), 0,
+                         m.stream, t);
     else
-      hipLaunchKernelGGL(k_vattn<64>, dim3(t.S, H), dim3(kAttnBlock), 0, m.stream, t);
+      hipLaunchKernelGGL((k_vattn<64, 5, 4, true>), dim3(t.S, H), dim3(attn_block<5>()), 0,
+                         m.stream, t);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     VMergeArgs mg{t.part_o, t.part_ml, actB, ka, t.S, hd, H, M};
     hipLaunchKernelGGL(k_vmerge, dim3(H, M), dim3(128), 0, m.stream, mg);

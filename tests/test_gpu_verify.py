@@ -17,6 +17,10 @@ CASES = {
     "hd128_gqa4": dict(n_heads=4, n_kv_heads=1, head_dim=128),
     "ragged": dict(d_model=320, ffn_dim=192, vocab=1000, n_heads=5, n_kv_heads=5),
     "int8": dict(wfmt="int8"),
+    # caches beyond 8K positions take the attention shape with two row
+    # groups, and 128 splits per head leave most splits empty
+    "long_cache": dict(max_ctx=8256),
+    "long_cache_hd128": dict(n_heads=4, n_kv_heads=1, head_dim=128, max_ctx=8256),
 }
 
 
@@ -40,7 +44,7 @@ def test_verify_equals_sequential_decode(name):
     try:
         P = cfg.prompt_len
         rng = np.random.default_rng(11)
-        for k in (0, 2, 4, 5, 8, 9):
+        for k in (0, 2, 3, 4, 5, 8, 9):
             token = int(rng.integers(0, cfg.vocab))
             drafts = rng.integers(0, cfg.vocab, k).astype(np.int32)
             kv_before = pair.kv_host.copy()
