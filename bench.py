@@ -488,6 +488,7 @@ def main() -> int:
             "value": round(cpu_tps, 4),
             "unit": "tokens/s",
             "cores": oracle.num_threads(),
+            "cpu_model": cpu_model(),
             "kind": "oracle",
             "sample": "first %d greedy decode steps from position %d of the same workload "
                       "(%.1f s)" % (n_done, P, c1 - c0),
@@ -503,6 +504,19 @@ def main() -> int:
         return 3
     print(json.dumps(result), flush=True)
     return 0
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or the platform's processor."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 if __name__ == "__main__":

@@ -54,7 +54,10 @@ enum {
   AIO_ERANGE = -2,       /* token or position out of range, k out of range  */
   AIO_EUNSUPPORTED = -3, /* shape or device this build does not handle      */
   AIO_EHIP = -4,         /* a HIP runtime or launch error; see aio_last_hip_error */
-  AIO_ENOMEM = -5        /* the library's own small allocations failed      */
+  AIO_ENOMEM = -5,       /* the library's own small allocations failed      */
+  AIO_EDEVICE = -6       /* a bounded wait inside the persistent decode kernel
+                            gave up (aio_device_status); the handle's results
+                            from then on are invalid: free it and load again */
 };
 
 /* Weight storage formats. */
@@ -136,7 +139,11 @@ int aio_last_hip_error(void);
 
 /* ---------------------------------------------------------- model lifecycle */
 
-/* Binds a model to caller-owned device memory.
+/* Binds a model to caller-owned device memory.  One handle is one resident
+ * model; the paper keeps its 1B probe and 7B backbone resident together in
+ * full precision and switches between them per request (Section 3.1,
+ * "System Architecture and Bandwidth Conservation"; Section 5.3), which here
+ * is two handles.
  *  cfg, w      host structs; copied.
  *  kv_dev      aio_kv_bytes(cfg) bytes; positions the caller has not written
  *              are never read before a decode or verify call writes them.
@@ -171,8 +178,13 @@ int aio_verify(aio_model* m, int32_t token, const int32_t* drafts, int32_t k, in
                float* logits_dev);
 
 /* Greedy argmax of `rows` rows of `n` fp32 values each (row-major), one
- * int32 index per row into out_dev.  The lowest index wins ties; NaN ranks
- * above +Inf (the first NaN wins).  rows in [1, max_verify], n in [1, 2^30]. */
+ * int32 index per row into out_dev: the next token of greedy decoding, and
+ * for a verify forward the per-row ids that prompt-lookup acceptance
+ * compares with the drafts (Section 3.3, Strategy Routing; Section 4.2, PLD
+ * Configuration).  The lowest index wins ties; NaN ranks above +Inf (the
+ * first NaN wins), as torch.argmax orders them.  logits_dev and out_dev
+ * 4-byte aligned.  AIO_ERANGE: rows outside [1, 65535] or n outside
+ * [1, 2^30]. */
 int aio_argmax(aio_model* m, const float* logits_dev, int32_t rows, int32_t n, int32_t* out_dev);
 
 /* Device-resident greedy decoding for timing: consume `token` at `pos`, then
@@ -239,7 +251,9 @@ int aio_tune_step(aio_model* m, int32_t token, int32_t pos, float* logits_dev, i
 
 /* Synchronises the model's stream and reports the device-side status word:
  * 0, or 1 if a bounded wait of the persistent kernel for another
- * workgroup's data gave up (its results are then invalid).  Synchronises. */
+ * workgroup's data gave up.  The word is sticky: once set, the results of
+ * that step and of every later call on the handle are invalid (free the
+ * handle and load again).  Synchronises. */
 int aio_device_status(aio_model* m, int32_t* status);
 
 /* ------------------------------------------ prompt-lookup decoding (host) */
@@ -282,7 +296,8 @@ typedef struct aio_pld_stats {
  * decoding produces from the same state, whatever the acceptance.
  * logits_dev (fp32 [k+1][vocab], 16-byte aligned) and argmax_dev (int32
  * [k+1]) are scratch.  stats may be NULL.  Synchronises the model's stream
- * once per round and returns when all n_new tokens are generated.
+ * once per round and returns when all n_new tokens are generated, or with
+ * AIO_EDEVICE as soon as a round finds the device status word set.
  * AIO_ERANGE: token outside [0, vocab), pos < 0, n_new < 1,
  * pos + n_new > max_ctx, k < 0, k + 1 > max_verify, ngram_min < 1 or
  * ngram_max < ngram_min.  AIO_EINVAL: a null pointer or a history token
@@ -342,7 +357,8 @@ typedef struct aio_spec_stats {
  * [k+1][vocab]), draft_logits_dev (fp32 [vocab]), argmax_dev (int32 [k+1])
  * and draft_tokens_dev (int32 [k]) are scratch, each 16-byte aligned (the
  * int32 buffers 4-byte aligned); stats may be NULL.  Synchronises both
- * models' streams twice per round.
+ * models' streams twice per round; returns AIO_EDEVICE as soon as either
+ * model's device status word is found set.
  * AIO_EINVAL: a null handle or buffer, or vocabularies that differ.
  * AIO_ERANGE: token outside [0, vocab), pos < 0, n_new < 1, pos + n_new
  * beyond either cache, k < 0 or k + 1 > the target's max_verify. */

@@ -15,7 +15,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libaio.so")
 
-AIO_OK, AIO_EINVAL, AIO_ERANGE, AIO_EUNSUPPORTED, AIO_EHIP, AIO_ENOMEM = 0, -1, -2, -3, -4, -5
+AIO_OK, AIO_EINVAL, AIO_ERANGE, AIO_EUNSUPPORTED, AIO_EHIP, AIO_ENOMEM, AIO_EDEVICE = \
+    0, -1, -2, -3, -4, -5, -6
 AIO_WFMT_BF16, AIO_WFMT_INT8 = 0, 1
 AIO_MAX_VERIFY_ROWS = 10
 LINEARS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
@@ -363,6 +364,13 @@ class DeviceModel:
         c = self.c
         t = self.kv.view(torch.int16).cpu().numpy().view(np.uint16)
         return t.reshape(c.n_layers, 2, c.n_kv_heads, c.max_ctx, c.head_dim)
+
+    def kv_rows(self, lo: int, hi: int) -> np.ndarray:
+        """Cache positions [lo, hi) as uint16 bf16 bits, [layer, K/V, kv head,
+        position, head_dim] (only those rows cross to the host)."""
+        c = self.c
+        t = self.kv.view(torch.int16).view(c.n_layers, 2, c.n_kv_heads, c.max_ctx, c.head_dim)
+        return t[:, :, :, lo:hi, :].cpu().numpy().view(np.uint16)
 
     def new_logits(self, rows: int = 1) -> torch.Tensor:
         return torch.empty((rows, self.c.vocab), dtype=torch.float32, device=self.device)

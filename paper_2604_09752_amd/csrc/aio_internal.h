@@ -30,6 +30,7 @@ struct WsLayout {
   size_t part_o;   // fp32 [MV][H][S][hd]     split-KV partial outputs
   size_t part_ml;  // fp32 [MV][H][S][2]      split-KV (max, sum) in log2 units
   size_t act;      // bf16 [2][32][KA]        split activations for the verify GEMM
+  size_t vpart;    // fp32 [kVerifyMaxKs][MV][d] verify residual products split over K
   size_t amax;     // int32 [MV]              argmax scratch
   size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters
   // step-kernel exchange buffers (tagged words), mega_xa .. mega_end zeroed at load
@@ -46,6 +47,10 @@ struct WsLayout {
   int mega_splits; // S_mega, split-KV partitions per kv head in the step kernel
   int ka;          // KA = max(d, H*hd, F)
 };
+
+// Largest number of K slices a verify residual product (O, down) is split
+// into; each slice's product goes to its own vpart slot.
+constexpr int kVerifyMaxKs = 8;
 
 WsLayout aio_ws_layout(const aio_config& c);
 

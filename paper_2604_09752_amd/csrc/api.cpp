@@ -69,6 +69,7 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.part_o = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * c.head_dim * 4);
   L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * 2 * 4);
   L.act = off; off = align256(off + 2 * 32 * ka * 2);  // two split-activation buffers
+  L.vpart = off; off = align256(off + (size_t)kVerifyMaxKs * MV * d * 4);
   L.amax = off; off = align256(off + MV * 4);
   L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
   L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
@@ -149,6 +150,7 @@ const char* aio_strerror(int code) {
     case AIO_EUNSUPPORTED: return "unsupported shape or device";
     case AIO_EHIP: return "HIP runtime error";
     case AIO_ENOMEM: return "out of host or device memory";
+    case AIO_EDEVICE: return "a bounded device-side wait gave up; the handle's results are invalid";
     default: return "unknown error";
   }
 }
@@ -575,6 +577,16 @@ int aio_device_status(aio_model* m, int32_t* status) {
 
 int aio_uses_step_kernel(const aio_model* m) { return m && m->use_mega ? 1 : 0; }
 
+// Enqueues a copy of the persistent kernel's status word into *word (0 for
+// handles that do not use that kernel); valid after the stream's next
+// synchronisation, which the generation loops make every round anyway.
+static hipError_t enqueue_status_copy(const aio_model* m, unsigned* word) {
+  *word = 0;
+  if (!m->use_mega) return hipSuccess;
+  return hipMemcpyAsync(word, m->ws + m->lay.sync + (size_t)kSyncErr * 4, 4,
+                        hipMemcpyDeviceToHost, m->stream);
+}
+
 // ---------------------------------------------------- the probe's front end
 
 int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev) {
@@ -661,10 +673,15 @@ int aio_spec_generate(aio_model* target, aio_model* draft, int32_t pos, int32_t 
     }
     if (rc) return rc;
     if ((rc = aio_argmax(target, target_logits_dev, kk + 1, ct.vocab, argmax_dev))) return rc;
+    unsigned bad_t = 0, bad_d = 0;
     e = hipMemcpyAsync(y, argmax_dev, (size_t)(kk + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
                        target->stream);
+    if (e == hipSuccess) e = enqueue_status_copy(target, &bad_t);
+    if (e == hipSuccess) e = enqueue_status_copy(draft, &bad_d);
     if (e == hipSuccess) e = hipStreamSynchronize(target->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(draft->stream);
     if (e != hipSuccess) return hip_fail(e);
+    if (bad_t || bad_d) return AIO_EDEVICE;
     int a = 0;
     while (a < kk && d[a] == y[a]) ++a;  // row a's argmax follows d[0..a)
     st.rounds += 1;
@@ -736,10 +753,13 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
                     : aio_decode_step(m, t, p, logits_dev);
     if (rc) return rc;
     if ((rc = aio_argmax(m, logits_dev, nd + 1, c.vocab, argmax_dev))) return rc;
+    unsigned bad = 0;
     hipError_t e = hipMemcpyAsync(y, argmax_dev, (size_t)(nd + 1) * sizeof(int32_t),
                                   hipMemcpyDeviceToHost, m->stream);
+    if (e == hipSuccess) e = enqueue_status_copy(m, &bad);
     if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
     if (e != hipSuccess) return hip_fail(e);
+    if (bad) return AIO_EDEVICE;
     int a = 0;
     while (a < nd && drafts[a] == y[a]) ++a;  // row a's argmax follows drafts[0..a)
     st.forwards += 1;

@@ -622,7 +622,9 @@ struct Smem {
 // Residual row u (tagged word) before a phase that adds to it: this
 // workgroup's own output of two phases back (O reads the DOWN output, or at
 // the first layer the embedding row stored at the start of the step; DOWN
-// reads the O output).  Same rows, same thread, so no wait.
+// reads the O output).  Same rows, same thread, so no wait.  Only rows past
+// a thread's first (more rows per workgroup than threads) read it: the
+// first row's exact value stays in the thread's register (k_step's xr).
 template <int KIND>
 AIO_DEV unsigned resid(const MegaArgs& a, int u) {
   return ld_dev((KIND == K_O ? a.xb : a.xa) + u);
@@ -681,7 +683,7 @@ AIO_DEV float fp16_hi(uint32_t w) { return fp16_to_f32((uint16_t)(w >> 16)); }
 // phase-specific output, stored with version `vo`.
 template <int WFMT, int KIND>
 AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, const float* red,
-                      Smem& sm, unsigned xpre, const EpiPre& pre, float inv, const Thr& T,
+                      Smem& sm, float& xr, const EpiPre& pre, float inv, const Thr& T,
                       unsigned vo, unsigned ep0) {
   constexpr int RPU = rpu_of<KIND>();
   const int nu = P.u1 - P.u0;
@@ -763,8 +765,12 @@ AIO_DEV void epilogue(const MegaArgs& a, const GPhase& P, int layer, int pos, co
         a.logits[u] = yy;
         if (am_better(yy, u, bv, bi)) { bv = yy; bi = u; }
       } else {
-        const float xo = untagf(t == tid ? xpre : resid<KIND>(a, u));
-        st_tag((KIND == K_O ? a.xa : a.xb) + u, xo + yy, vo);
+        // the thread's first row keeps its exact value in xr; only the
+        // copy handed to other workgroups carries the version tag
+        const float xo = t == tid ? xr : untagf(resid<KIND>(a, u));
+        const float xn = xo + yy;
+        if (t == tid) xr = xn;
+        st_tag((KIND == K_O ? a.xa : a.xb) + u, xn, vo);
       }
     }
   }
@@ -812,7 +818,7 @@ struct Bufs {
 // soon as it is consumed.
 template <int WFMT, int HD, int KIND, int VPL>
 AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& W, float* lds,
-                        Smem& sm, unsigned ep0, unsigned k) {
+                        Smem& sm, unsigned ep0, unsigned k, float& xr) {
   constexpr int RPU = rpu_of<KIND>();
   // LDS partials and norm sums alternate between two buffers by phase
   // parity: a wave may start this phase while another still reads the
@@ -824,14 +830,6 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
   const int nb = (P.u1 - P.u0 + UB - 1) / UB;
   const unsigned slot = KIND == K_LM ? 0u : k;  // timing slot
   const Thr T = thr();
-  // residual rows this workgroup will update, fetched now to hide the trip
-  // (unconditionally, and kept tagged until the epilogue: a load under a
-  // branch, or an early use, would be waited for here behind batch 0)
-  unsigned xpre = 0u;
-  if (KIND == K_O || KIND == K_DOWN) {
-    const int t = T.tid < P.u1 - P.u0 ? T.tid : 0;
-    xpre = resid<KIND>(a, P.u0 + t < a.d ? P.u0 + t : a.d - 1);
-  }
   EpiPre pre;
   {
     const int t = T.tid < P.u1 - P.u0 ? T.tid : 0;
@@ -875,7 +873,7 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
     for (int w = 0; w < kW; ++w) tot += ss8[w];
     inv = rsqrtf(tot / (float)P.K + a.eps);
   }
-  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xpre, pre, inv, T, ver_of(ep0, k), ep0);
+  epilogue<WFMT, KIND>(a, P, layer, pos, red, sm, xr, pre, inv, T, ver_of(ep0, k), ep0);
   if (KIND != K_LM) {
     // A workgroup's memory requests leave its CU in the order they were
     // issued, by whatever wave.  The outputs are stored by the first waves
@@ -1236,31 +1234,39 @@ __global__ __launch_bounds__(kT, 1) void k_step(MegaArgs a) {
   Bufs W;
   KV4 X, Y;
   prefetch<WFMT, HD, K_QKV, VQ>(a, 0, W);
+  // The residual stream of this thread's first row of the O and down
+  // projections (both split the d rows the same way), kept exact in a
+  // register for the whole step: handing it between workgroups costs its
+  // 3 low mantissa bits (the version tag), which would otherwise accumulate
+  // over the 2 L additions.
+  float xr = 0.f;
   {
     // the residual before layer 0 (the embedding row) of the rows this
     // workgroup updates in the O projection
     const GPhase P = make_phase<WFMT, K_O>(a, 0);
     const int t = thr().tid;
-    if (t < P.u1 - P.u0)
-      st_tag(a.xb + P.u0 + t, bf16_to_f32(a.embed[(size_t)token * a.d + P.u0 + t]), ver_of(ep0, 0));
+    if (t < P.u1 - P.u0) {
+      xr = bf16_to_f32(a.embed[(size_t)token * a.d + P.u0 + t]);
+      st_tag(a.xb + P.u0 + t, xr, ver_of(ep0, 0));
+    }
   }
   for (int l = 0; l < a.L; ++l) {
     const unsigned k = 5u * (unsigned)l;
-    gemv_phase<WFMT, HD, K_QKV, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 1);
+    gemv_phase<WFMT, HD, K_QKV, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 1, xr);
     attn_prefetch<HD>(a, l, pos, X, Y);
     attn_phase<HD, G>(a, l, pos, X, Y, lds + 2 * a.red_words, sm, ep0, k + 2);
     prefetch<WFMT, HD, K_O, VQ>(a, l, W);
-    gemv_phase<WFMT, HD, K_O, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 3);
+    gemv_phase<WFMT, HD, K_O, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 3, xr);
     prefetch<WFMT, HD, K_GU, VQ>(a, l, W);
-    gemv_phase<WFMT, HD, K_GU, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 4);
+    gemv_phase<WFMT, HD, K_GU, VQ>(a, l, pos, token, W, lds, sm, ep0, k + 4, xr);
     prefetch<WFMT, HD, K_DOWN, VD>(a, l, W);
-    gemv_phase<WFMT, HD, K_DOWN, VD>(a, l, pos, token, W, lds, sm, ep0, k + 5);
+    gemv_phase<WFMT, HD, K_DOWN, VD>(a, l, pos, token, W, lds, sm, ep0, k + 5, xr);
     if (l + 1 < a.L)
       prefetch<WFMT, HD, K_QKV, VQ>(a, l + 1, W);
     else
       prefetch<WFMT, HD, K_LM, VQ>(a, l + 1, W);
   }
-  gemv_phase<WFMT, HD, K_LM, VQ>(a, a.L, pos, token, W, lds, sm, ep0, 5u * (unsigned)a.L + 1);
+  gemv_phase<WFMT, HD, K_LM, VQ>(a, a.L, pos, token, W, lds, sm, ep0, 5u * (unsigned)a.L + 1, xr);
 }
 
 // The grid is one workgroup per CU and a CU holds at most one (registers

@@ -23,8 +23,6 @@
 
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / AIO_WAVE;
 // The skinny GEMM runs 8 waves per workgroup: more weight loads in flight
 // per CU, and the K range of a workgroup split eight ways.
 constexpr int kGBlock = 512;
@@ -56,9 +54,10 @@ AIO_DEV void store_split(uint16_t* act, int lda, int M, int r, int col, float v)
 // ------------------------------------------------------------ RMSNorm rows
 
 struct VNormArgs {
-  const float* x;           // [M][d] residual rows
+  float* x;                 // [M][d] residual rows
   const uint16_t* embed;    // layer 0: embedding table (tokens from state), else null
-  float* x_copy;            // layer 0: x rows written from the embedding
+  const float* part;        // [nparts][M][d] K-slice products still to add to x, or null
+  int nparts;
   const uint16_t* gain;
   uint16_t* act;            // [32][lda] split output
   int lda, d, M;
@@ -69,6 +68,11 @@ struct VNormArgs {
 // One workgroup of 1024 threads per row r: h = x_r / sqrt(mean(x_r^2) + eps)
 // * g, split.  Each thread keeps up to kNormVals of its elements in
 // registers between the two passes (all of them for d <= 8192).
+//
+// The row x_r is first completed: in layer 0 it is the embedding row of the
+// row's token; after a residual product that was split over K it is x_r plus
+// the slices' products, added in slice order, so the sum (and everything
+// after it) is the same on every run.  The completed row is written back.
 constexpr int kNormBlock = 1024;
 constexpr int kNormVals = 8;
 
@@ -76,8 +80,14 @@ __global__ __launch_bounds__(kNormBlock) void k_vnorm(VNormArgs a) {
   __shared__ float red[kNormBlock / AIO_WAVE];
   const int r = blockIdx.x, tid = threadIdx.x;
   const uint16_t* emb = a.embed ? a.embed + (size_t)a.st->token[r] * a.d : nullptr;
-  const float* xr = a.x + (size_t)r * a.d;
-  auto val = [&](int e) { return emb ? bf16_to_f32(emb[e]) : xr[e]; };
+  float* xr = a.x + (size_t)r * a.d;
+  const bool write_x = emb || a.nparts > 0;
+  auto val = [&](int e) {
+    if (emb) return bf16_to_f32(emb[e]);
+    float v = xr[e];
+    for (int s = 0; s < a.nparts; ++s) v += a.part[((size_t)s * a.M + r) * a.d + e];
+    return v;
+  };
   float v[kNormVals];
   float ss = 0.f;
 #pragma unroll
@@ -98,7 +108,7 @@ __global__ __launch_bounds__(kNormBlock) void k_vnorm(VNormArgs a) {
   for (int w = 0; w < kNormBlock / AIO_WAVE; ++w) tot += red[w];
   const float inv = rsqrtf(tot / (float)a.d + a.eps);
   auto out = [&](int e, float x) {
-    if (emb) a.x_copy[(size_t)r * a.d + e] = x;
+    if (write_x) xr[e] = x;
     store_split(a.act, a.lda, a.M, r, e, x * inv * bf16_to_f32(a.gain[e]));
   };
 #pragma unroll
@@ -131,6 +141,7 @@ struct VGemmArgs {
   const aio_state* st;
   int H, Hkv, hd, max_ctx;
   int ks;                   // K splits across workgroups (grid.y); > 1 only for EPI_RESID
+  float* part;              // RESID with ks > 1: [ks][M][ldo], slice y's product
 };
 
 // The k of the two MFMA fragments a lane holds in a block of 32 k (lane
@@ -419,8 +430,9 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
         float v = y[t];
         if constexpr (WFMT == AIO_WFMT_INT8) v *= fp16_to_f32(a.s0[n]);
         if constexpr (EPI == EPI_RESID) {
-          // K split over workgroups: each adds its part of the product
-          if (a.ks > 1) unsafeAtomicAdd(a.out + (size_t)r * a.ldo + n, v);
+          // K split over workgroups: each slice stores its part of the
+          // product, and the next RMSNorm adds the parts in slice order
+          if (a.ks > 1) a.part[((size_t)blockIdx.y * M + r) * a.ldo + n] = v;
           else a.out[(size_t)r * a.ldo + n] += v;
         } else {
           a.out[(size_t)r * a.ldo + n] = v;
@@ -644,15 +656,21 @@ __global__ __launch_bounds__(128) void k_vmerge(VMergeArgs a) {
 
 // Launch with `blocks` tile pairs.  A residual-add product with fewer tile
 // pairs than CUs also splits K over workgroups, as far as every wave keeps
-// at least two blocks of 32 k; the others run one K slice per workgroup.
+// at least two blocks of 32 k (at most kVerifyMaxKs slices); the others run
+// one K slice per workgroup.  *ks_out receives the slice count: with more
+// than one, the slices' products are in the vpart region, still to be added.
 template <int EPI>
-hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
+hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks, int* ks_out = nullptr) {
   VGemmArgs a = g;
   a.ks = 1;
   if (EPI == EPI_RESID) {
     const int nkb = a.K / 32;
-    while (blocks * a.ks < m.num_cus && nkb / (2 * a.ks * kGWaves) >= 2) a.ks *= 2;
+    while (blocks * a.ks < m.num_cus && 2 * a.ks <= kVerifyMaxKs &&
+           nkb / (2 * a.ks * kGWaves) >= 2)
+      a.ks *= 2;
+    a.part = m.at<float>(m.lay.vpart);
   }
+  if (ks_out) *ks_out = a.ks;
   const dim3 grid(blocks, a.ks);
   if (m.cfg.wfmt == AIO_WFMT_INT8)
     hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), grid, dim3(kGBlock), 0, m.stream, a);
@@ -661,12 +679,15 @@ hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
   return hipGetLastError();
 }
 
-hipError_t launch_vnorm(const aio_model& m, const float* x, const uint16_t* embed, const void* gain,
-                        uint16_t* act, int M) {
+// RMSNorm of the M rows of x; `nparts` K-slice products (vpart) are first
+// added to x (launch_vgemm's slice count, or 0).
+hipError_t launch_vnorm(const aio_model& m, float* x, const uint16_t* embed, const void* gain,
+                        uint16_t* act, int M, int nparts) {
   VNormArgs n{};
   n.x = x;
   n.embed = embed;
-  n.x_copy = m.at<float>(m.lay.x);
+  n.part = m.at<float>(m.lay.vpart);
+  n.nparts = nparts > 1 ? nparts : 0;
   n.gain = (const uint16_t*)gain;
   n.act = act;
   n.lda = m.lay.ka;
@@ -691,9 +712,11 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
   float* x = m.at<float>(m.lay.x);
   float* q = m.at<float>(m.lay.q);
   hipError_t e;
+  int pend = 0;  // K slices of the last residual product not yet added to x
   for (int l = 0; l < c.n_layers; ++l) {
     const aio_layer_weights& L = m.layers[(size_t)l];
-    e = launch_vnorm(m, x, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm, actA, M);
+    e = launch_vnorm(m, x, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm, actA, M,
+                     pend);
     if (e != hipSuccess) return e;
 
     VGemmArgs g{};
@@ -737,9 +760,9 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     o.act = actB; o.lda = ka; o.M = M;
     o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
     o.N = d; o.K = H * hd; o.out = x; o.ldo = d; o.st = m.state();
-    if ((e = launch_vgemm<EPI_RESID>(m, o, (d + 63) / 64)) != hipSuccess) return e;
+    if ((e = launch_vgemm<EPI_RESID>(m, o, (d + 63) / 64, &pend)) != hipSuccess) return e;
 
-    if ((e = launch_vnorm(m, x, nullptr, L.ffn_norm, actA, M)) != hipSuccess) return e;
+    if ((e = launch_vnorm(m, x, nullptr, L.ffn_norm, actA, M, pend)) != hipSuccess) return e;
     VGemmArgs gu{};
     gu.act = actA; gu.lda = ka; gu.M = M;
     gu.w0 = L.w_gate; gu.w1 = L.w_up;
@@ -751,9 +774,9 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     dn.act = actB; dn.lda = ka; dn.M = M;
     dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
     dn.N = d; dn.K = F; dn.out = x; dn.ldo = d; dn.st = m.state();
-    if ((e = launch_vgemm<EPI_RESID>(m, dn, (d + 63) / 64)) != hipSuccess) return e;
+    if ((e = launch_vgemm<EPI_RESID>(m, dn, (d + 63) / 64, &pend)) != hipSuccess) return e;
   }
-  if ((e = launch_vnorm(m, x, nullptr, m.final_norm, actA, M)) != hipSuccess) return e;
+  if ((e = launch_vnorm(m, x, nullptr, m.final_norm, actA, M, pend)) != hipSuccess) return e;
   VGemmArgs lm{};
   lm.act = actA; lm.lda = ka; lm.M = M;
   lm.w0 = m.lm_head; lm.s0 = (const uint16_t*)m.s_lm_head;

@@ -51,11 +51,15 @@ def rmsnorm_rows(X: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
     return X / np.sqrt(np.mean(X * X, axis=-1, keepdims=True) + eps) * g
 
 
-def full_causal_logits(cfg, w: dict, toks: np.ndarray) -> np.ndarray:
+def full_causal_logits(cfg, w: dict, toks: np.ndarray, hand_over=None) -> np.ndarray:
     """Logits at every position of ``toks`` with one causal-masked forward.
 
     K and V are rounded to bf16 (through fp32) before use, as the cache holds
-    them.  Returns fp64 [T][V]."""
+    them.  ``hand_over``, if given, is applied to every activation a fused
+    decode step passes from one group of workers to the next (the residual
+    stream after each addition, the rotated queries, the attention output,
+    the SwiGLU product).  Returns fp64 [T][V]."""
+    ho = hand_over if hand_over is not None else (lambda a: a)
     T = len(toks)
     d, H, Hkv, hd = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
     G = H // Hkv
@@ -68,7 +72,7 @@ def full_causal_logits(cfg, w: dict, toks: np.ndarray) -> np.ndarray:
         Q = (Hn @ dense(w, p + "wq", cfg.wfmt).T).reshape(T, H, hd)
         K = (Hn @ dense(w, p + "wk", cfg.wfmt).T).reshape(T, Hkv, hd)
         Vv = (Hn @ dense(w, p + "wv", cfg.wfmt).T).reshape(T, Hkv, hd)
-        Q = apply_rope(Q, cos, sin)
+        Q = ho(apply_rope(Q, cos, sin))
         K = round_bf16(apply_rope(K, cos, sin))
         Vv = round_bf16(Vv)
         O = np.empty((T, H, hd))
@@ -79,11 +83,11 @@ def full_causal_logits(cfg, w: dict, toks: np.ndarray) -> np.ndarray:
             A = np.exp(S)
             A /= A.sum(axis=1, keepdims=True)
             O[:, h, :] = A @ Vv[:, h // G, :]
-        X = X + O.reshape(T, H * hd) @ dense(w, p + "wo", cfg.wfmt).T
+        X = ho(X + ho(O).reshape(T, H * hd) @ dense(w, p + "wo", cfg.wfmt).T)
         H2 = rmsnorm_rows(X, bf16_to_f64(w[p + "ffn_norm"]), cfg.rms_eps)
         Gt = H2 @ dense(w, p + "w_gate", cfg.wfmt).T
         Up = H2 @ dense(w, p + "w_up", cfg.wfmt).T
-        M = Gt / (1.0 + np.exp(-Gt)) * Up
-        X = X + M @ dense(w, p + "w_down", cfg.wfmt).T
+        M = ho(Gt / (1.0 + np.exp(-Gt)) * Up)
+        X = ho(X + M @ dense(w, p + "w_down", cfg.wfmt).T)
     Hf = rmsnorm_rows(X, bf16_to_f64(w["final_norm"]), cfg.rms_eps)
     return Hf @ dense(w, "lm_head", cfg.wfmt).T

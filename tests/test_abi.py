@@ -106,7 +106,7 @@ def test_verify_ranges(L):
 
 
 def test_strerror(L):
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert B.aio_strerror(code)
     assert B.aio_strerror(-99) == "unknown error"
 
