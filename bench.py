@@ -177,9 +177,13 @@ def dual_bench(r: int, rounds: int = 8) -> int:
 def probe_bench(n: int, reps: int = 5) -> int:
     """The probe's front end (Section 3.2): the 1B-class decoder consumes an
     n-token request (seeded random tokens standing in for the templated
-    prompt) from position 0 through the verify forward in chunks, then the
-    routing rule reads the logits of three seeded label tokens.  The paper
-    measures 11.8 ms for its probe's prefill (Section 5.3)."""
+    prompt) from position 0 in prompt-length matrix products (aio_prefill),
+    then the routing rule reads the logits of three seeded label tokens.  The
+    paper measures 11.8 ms for its probe's prefill (Section 5.3).  Reported
+    besides the time: the algorithmic flops of the prefill (2 n x the linear
+    parameters, causal attention, the last row's LM head) per second, and the
+    MFMA rate (the products run on two bf16 terms of every activation, twice
+    the algorithmic flops of the linear layers)."""
     import torch
     import synth
     from paper_2604_09752_amd import binding
@@ -203,8 +207,16 @@ def probe_bench(n: int, reps: int = 5) -> int:
     t0 = time.perf_counter()
     small, h, cat = binding.aio_probe_route(cat_logits, 0, n)
     route_us = (time.perf_counter() - t0) * 1e6
+    d, hd, L = cfg.d_model, cfg.head_dim, cfg.n_layers
+    lin = L * (d * cfg.n_heads * hd + 2 * d * cfg.n_kv_heads * hd + cfg.n_heads * hd * d
+               + 3 * d * cfg.ffn_dim)
+    attn = 4 * L * cfg.n_heads * hd * (n * (n + 1) // 2)
+    flops = 2 * n * lin + attn + 2 * cfg.vocab * d
     out = {"request_tokens": n, "prefill_ms": round(ms, 3),
-           "prefill_chunks": -(-n // cfg.max_verify), "entropy_nats": round(h, 4), "category": cat,
+           "tokens_per_s": round(n / ms * 1e3, 1),
+           "algorithmic_tflops": round(flops / ms / 1e9, 1),
+           "mfma_tflops": round((4 * n * lin + 2 * attn) / ms / 1e9, 1),
+           "entropy_nats": round(h, 4), "category": cat,
            "route_to_small_model": small, "route_decision_us": round(route_us, 1),
            "workload": workload_name(cfg)}
     rc = 3 if dm.status() != 0 else 0

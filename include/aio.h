@@ -308,14 +308,21 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
 
 /* -------------------------------------------- the probe's front end (host) */
 
-/* Consumes tokens[0..n) (host) at positions pos .. pos+n-1 through the verify
- * forward, in chunks of max_verify rows (Section 3.2, "Probe-Based
- * Request-Level Intent Sensing": the probe runs one forward over the
- * templated request).  Writes every token's K/V; logits_dev (fp32
- * [max_verify][vocab], 16-byte aligned) is scratch, and on return its row 0
- * holds the logits after the last token.  Asynchronous like aio_verify.
+/* The probe's single forward over its templated request (Section 3.2,
+ * "Probe-Based Request-Level Intent Sensing"; its cost is the "1B
+ * Single-Token Prefill" of Section 5.3): consumes tokens[0..n) (host) at
+ * positions pos .. pos+n-1 in prompt-length matrix products (up to 2048
+ * rows per pass over the weights) with causal attention, writes every
+ * token's K/V in every layer, and writes the logits after the last token,
+ * fp32 [vocab], to logits_dev (16-byte aligned).  The result equals n
+ * aio_decode_step calls up to rounding.  The scratch
+ * (4 (1 + d + H hd + max(d, H hd) + F) bytes per row, for up to 2048 rows) is allocated by
+ * the library on the first call that needs more and kept until
+ * aio_model_free, so such a call synchronises once.  Asynchronous
+ * otherwise, like aio_verify.
  * AIO_ERANGE: n < 1, pos < 0, pos + n > max_ctx or a token outside
- * [0, vocab); AIO_EINVAL: a null pointer. */
+ * [0, vocab); AIO_EINVAL: a null pointer; AIO_ENOMEM: the scratch could not
+ * be allocated. */
 int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev);
 
 /* The probe's routing decision (Section 3.2 and Section 3.3, "Dynamic

@@ -397,8 +397,8 @@ class DeviceModel:
                                 logits, am)
 
     def prefill(self, tokens, pos: int, logits: torch.Tensor) -> None:
-        """Consume tokens at pos.. through the verify forward; row 0 of logits
-        (max_verify rows) ends with the last token's logits."""
+        """Consume tokens at pos.. in prompt-length matrix products; logits
+        (fp32, at least [vocab]) receives the last token's logits."""
         t = np.ascontiguousarray(tokens, dtype=np.int32)
         _check(lib().aio_prefill(self.handle, t.ctypes.data, int(t.size), int(pos), _ptr(logits)),
                "aio_prefill")

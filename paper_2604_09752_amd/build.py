@@ -16,7 +16,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libaio.so")
-SOURCES = ["api.cpp", "decode_kernels.hip", "verify_kernels.hip", "step_kernel.hip"]
+SOURCES = ["api.cpp", "decode_kernels.hip", "verify_kernels.hip", "step_kernel.hip",
+           "prefill_kernels.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

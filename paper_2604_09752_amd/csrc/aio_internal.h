@@ -79,6 +79,9 @@ struct aio_model {
   int* gu_bounds_dev;              // library-owned [mega_blocks + 1] gate/up unit bounds
   std::vector<int> gu_bounds;      // host copy
   unsigned long long* mega_trace;  // library-owned, allocated on first trace
+  // prefill scratch (aio_prefill), library-owned, grown on demand
+  char* pf_scratch;
+  int pf_rcap;
   // profiling: when prof_ev is set, every launcher records one event after
   // each kernel it enqueues (aio_profile_step)
   mutable hipEvent_t* prof_ev;
@@ -110,3 +113,25 @@ hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, 
 
 // ---- launchers (verify_kernels.hip) ----
 hipError_t aio_launch_verify(const aio_model& m, int rows, float* logits);
+// Final RMSNorm and LM head of the first `rows` rows of the workspace's
+// residual rows (lay.x): logits [rows][vocab].
+hipError_t aio_launch_lm_rows(const aio_model& m, int rows, float* logits);
+
+// ---- prefill (prefill_kernels.hip) ----
+// Scratch of one prefill chunk of up to rcap prompt rows.
+struct PfBuffers {
+  int32_t* tokens;  // [rcap]
+  float* x;         // [rcap][d] residual rows
+  float* q;         // [rcap][H hd] rotated queries
+  uint16_t* actA;   // [2][rcap][lda_a] split activations: QKV, O and gate/up inputs
+  uint16_t* actB;   // [2][rcap][lda_b] split SwiGLU output: the down input
+  int rcap, lda_a, lda_b;
+  size_t bytes;     // total, every region 256-byte aligned
+};
+// Scratch bytes per prompt row (without alignment padding).
+size_t aio_prefill_row_bytes(const aio_config& c);
+// The chunk scratch laid out from `base` (null: only .bytes is meaningful).
+PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap);
+// One chunk of R <= b.rcap rows (tokens already in b.tokens) at positions
+// pos0 .. pos0 + R - 1.
+hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int R, int pos0);

@@ -288,6 +288,7 @@ void aio_model_free(aio_model* m) {
   if (m->mega_layers) (void)hipFree(m->mega_layers);
   if (m->gu_bounds_dev) (void)hipFree(m->gu_bounds_dev);
   if (m->mega_trace) (void)hipFree(m->mega_trace);
+  if (m->pf_scratch) (void)hipFree(m->pf_scratch);
   delete m;
 }
 
@@ -589,26 +590,64 @@ static hipError_t enqueue_status_copy(const aio_model* m, unsigned* word) {
 
 // ---------------------------------------------------- the probe's front end
 
-int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev) {
+// Rows of one prefill chunk when the library sizes the scratch: the whole
+// prompt up to this many rows, in multiples of the GEMM's 64-row tiles.
+constexpr int kPrefillChunk = 2048;
+
+// Checks shared by the prefill entry points.
+static int check_prefill(const aio_model* m, const int32_t* tokens, int32_t n, int32_t pos,
+                         const float* logits_dev) {
   if (!m || !tokens || !logits_dev || !aligned16(logits_dev)) return AIO_EINVAL;
   const aio_config& c = m->cfg;
   if (n < 1 || pos < 0 || (int64_t)pos + n > c.max_ctx) return AIO_ERANGE;
   for (int32_t i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c.vocab) return AIO_ERANGE;
+  return AIO_OK;
+}
+
+// Enqueues the prompt in chunks of at most b.rcap rows, then the last row's
+// final RMSNorm and LM head into logits_dev.
+static hipError_t enqueue_prefill(aio_model* m, const PfBuffers& b, const int32_t* tokens,
+                                  int32_t n, int32_t pos, float* logits_dev) {
+  const int d = m->cfg.d_model;
   int32_t done = 0, rows = 0;
-  while (done < n) {
-    rows = std::min(n - done, c.max_verify);
-    const int rc = aio_verify(m, tokens[done], tokens + done + 1, rows - 1, pos + done, logits_dev);
-    if (rc) return rc;
+  hipError_t e = hipSuccess;
+  while (done < n && e == hipSuccess) {
+    rows = std::min(n - done, b.rcap);
+    e = hipMemcpyAsync(b.tokens, tokens + done, (size_t)rows * sizeof(int32_t),
+                       hipMemcpyHostToDevice, m->stream);
+    if (e == hipSuccess) e = aio_launch_prefill_chunk(*m, b, rows, pos + done);
     done += rows;
   }
-  if (rows > 1) {  // the last row's logits to row 0
-    const hipError_t e = hipMemcpyAsync(logits_dev, logits_dev + (size_t)(rows - 1) * c.vocab,
-                                        (size_t)c.vocab * sizeof(float), hipMemcpyDeviceToDevice,
-                                        m->stream);
-    if (e != hipSuccess) return hip_fail(e);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(m->at<float>(m->lay.x), b.x + (size_t)(rows - 1) * d,
+                       (size_t)d * sizeof(float), hipMemcpyDeviceToDevice, m->stream);
+  if (e == hipSuccess) e = aio_launch_lm_rows(*m, 1, logits_dev);
+  return e;
+}
+
+int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev) {
+  int rc = check_prefill(m, tokens, n, pos, logits_dev);
+  if (rc) return rc;
+  const int want = std::min((n + 63) / 64 * 64, kPrefillChunk);
+  if (m->pf_rcap < want) {
+    // grow the library-owned scratch (synchronous; later calls reuse it)
+    hipError_t e = hipSuccess;
+    if (m->pf_scratch) e = hipStreamSynchronize(m->stream);
+    if (e == hipSuccess && m->pf_scratch) e = hipFree(m->pf_scratch);
+    m->pf_scratch = nullptr;
+    m->pf_rcap = 0;
+    if (e == hipSuccess)
+      e = hipMalloc((void**)&m->pf_scratch, aio_prefill_buffers(m->cfg, nullptr, want).bytes);
+    if (e != hipSuccess) {
+      m->pf_scratch = nullptr;
+      return e == hipErrorOutOfMemory ? AIO_ENOMEM : hip_fail(e);
+    }
+    m->pf_rcap = want;
   }
-  return AIO_OK;
+  const PfBuffers b = aio_prefill_buffers(m->cfg, m->pf_scratch, m->pf_rcap);
+  const hipError_t e = enqueue_prefill(m, b, tokens, n, pos, logits_dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
 }
 
 int aio_probe_route(const float* category_logits, int32_t n_categories, int32_t code_category,

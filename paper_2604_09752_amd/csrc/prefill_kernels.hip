@@ -1,0 +1,741 @@
+// Prefill: a prompt of R rows at positions pos0 .. pos0 + R - 1 in one pass
+// of prompt-length matrix products (M = R), for gfx950.  This is the probe's
+// single forward over its templated request: every row's K and V go to the
+// cache, and the last row's logits come out.
+//
+// Per layer: pnorm (RMSNorm + split) -> QKV GEMM (+RoPE, K/V append) ->
+// pattn (causal flash attention; row r sees positions [0, pos0 + r]; its
+// output split) -> O GEMM (+residual) -> pnorm -> gate/up GEMM (+SwiGLU,
+// split) -> down GEMM (+residual).  The last row then goes through the final
+// RMSNorm and the LM head of the verify path.
+//
+// Precision.  Activations stay fp32 between kernels.  The GEMMs run on MFMA
+// (v_mfma_f32_32x32x16_bf16) with every activation split exactly into three
+// bf16 terms, a = t0 + t1 + t2 + r with |r| <= 2^-27 |a|, so the products
+// keep fp32 accuracy (two terms leave 2^-18, which measurably loosens the
+// cache rows of deeper layers).  Weights are exact in bf16 (int8 weights
+// convert exactly; their fp16 per-output-channel scale applies in the
+// epilogue).  Attention splits the queries and the softmax weights into
+// three terms as well.
+#include <math.h>
+
+#include "aio_internal.h"
+#include "common.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+AIO_DEV f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+AIO_DEV bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+// Terms of the activation split.
+constexpr int kNT = 3;
+
+// Exact three-term bf16 split: t0 = bf16(a), t1 = bf16(a - t0),
+// t2 = bf16(a - t0 - t1) (each subtraction is exact in fp32).
+AIO_DEV void split3(float a, uint16_t& t0, uint16_t& t1, uint16_t& t2) {
+  t0 = f32_to_bf16(a);
+  const float r1 = a - bf16_to_f32(t0);
+  t1 = f32_to_bf16(r1);
+  t2 = f32_to_bf16(r1 - bf16_to_f32(t1));
+}
+
+// The split of `a` into the term planes p[0], p[ts], p[2 ts].
+AIO_DEV void store_terms(uint16_t* p, size_t ts, float a) { split3(a, p[0], p[ts], p[2 * ts]); }
+
+// Wait for this wave's LDS operations; also a compiler barrier, so no LDS
+// access moves across it.  Lanes of one wave exchange data through LDS
+// without a workgroup barrier (the waves of a workgroup run different
+// numbers of iterations).
+AIO_DEV void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// ------------------------------------------------------------- RMSNorm rows
+
+struct PNormArgs {
+  float* x;                // [R][d] residual rows (layer 0: written from the embedding)
+  const uint16_t* embed;   // layer 0: embedding table, else null
+  const int32_t* tokens;   // [R] (layer 0)
+  const uint16_t* gain;
+  uint16_t* act;           // [kNT][R][lda]: terms of the normalised rows
+  int lda;
+  size_t tstride;          // elements between term planes
+  int d;
+  float eps;
+};
+
+constexpr int kNormThreads = 256;
+
+// One workgroup per row: h = x / sqrt(mean(x^2) + eps) * g, split.
+__global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
+  __shared__ float red[kNormThreads / AIO_WAVE];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  float* xr = a.x + (size_t)r * a.d;
+  const uint16_t* emb = a.embed ? a.embed + (size_t)a.tokens[r] * a.d : nullptr;
+  float ss = 0.f;
+  for (int e = tid; e < a.d; e += kNormThreads) {
+    float v;
+    if (emb) {
+      v = bf16_to_f32(emb[e]);
+      xr[e] = v;
+    } else {
+      v = xr[e];
+    }
+    ss = fmaf(v, v, ss);
+  }
+  ss = wave_sum(ss);
+  if ((tid & (AIO_WAVE - 1)) == 0) red[tid / AIO_WAVE] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormThreads / AIO_WAVE; ++w) tot += red[w];
+  const float inv = rsqrtf(tot / (float)a.d + a.eps);
+  uint16_t* out = a.act + (size_t)r * a.lda;
+  for (int e = tid; e < a.d; e += kNormThreads) {
+    const float v = (emb ? bf16_to_f32(emb[e]) : xr[e]) * inv * bf16_to_f32(a.gain[e]);
+    store_terms(out + e, a.tstride, v);
+  }
+}
+
+// --------------------------------------------------------------------- GEMM
+
+// A workgroup of 4 waves computes a tile of 128 weight rows (4 blocks of
+// 32) by 64 prompt rows, every term of each.  Wave (wn, wr) owns row blocks
+// 2 wn ("lo") and 2 wn + 1 ("hi") and prompt rows [32 wr, 32 wr + 32), so the
+// two rows an epilogue combines (a RoPE pair, gate and up) sit in one lane.
+// Weights and activations pass through LDS in stages of 32 k, double
+// buffered: the next stage's global loads are in flight in registers while
+// the current one is multiplied.  Rows in LDS are 80 bytes apart (64 + a
+// 16-byte skew), so the 32 rows a fragment read touches spread over the
+// banks.
+constexpr int kGT = 256;
+constexpr int kBM = 128;  // weight rows per tile
+constexpr int kBR = 64;   // prompt rows per tile
+constexpr int kKT = 32;   // k per stage
+constexpr int kRowB = kKT * 2 + 16;
+constexpr int kBCols = kNT * kBR;                  // activation columns: term-major per wave half
+constexpr int kStageB = (kBM + kBCols) * kRowB;    // weight rows + activation columns
+constexpr int kGemmLds = 2 * kStageB;
+constexpr int kBLd = kBCols * (kKT / 8) / kGT;     // 16-byte activation loads per thread
+static_assert(kBCols * (kKT / 8) % kGT == 0, "activation stage must split evenly");
+
+enum PEpi { PE_QKV = 0, PE_RESID = 1, PE_SWIGLU = 2 };
+
+struct PGemmArgs {
+  const uint16_t* act;  // [kNT][R][lda] split activations
+  int lda;
+  size_t tstride;
+  int R;
+  const void* w0;       // QKV: wq | SWIGLU: w_gate | RESID: the matrix
+  const void* w1;       // QKV: wk | SWIGLU: w_up
+  const void* w2;       // QKV: wv
+  const uint16_t* s0;
+  const uint16_t* s1;
+  const uint16_t* s2;
+  int N, K;             // QKV: N = (H + 2 Hkv) hd virtual rows; SWIGLU: F; RESID: rows
+  float* out;           // QKV: q [R][H hd] | RESID: x [R][N]
+  int ldo;
+  uint16_t* act_out;    // SWIGLU: [kNT][R][lda_out]
+  int lda_out;
+  size_t tstride_out;
+  uint16_t* kc;         // QKV: cache of the layer, [Hkv][max_ctx][hd]
+  uint16_t* vc;
+  const float2* rope;   // [max_ctx][hd / 2] (cos, sin)
+  int pos0, H, Hkv, hd, max_ctx;
+};
+
+// Where block `blk` (0..3) of tile `bx` reads its 32 rows: matrix index
+// (0, 1, 2 = w0, w1, w2), first row in that matrix, and the number of valid
+// rows (0 for a block past the end).
+struct BlockSrc {
+  int mat, row0, valid;
+  int vrow0;  // QKV: virtual row of the block's first row
+};
+
+template <int EPI>
+AIO_DEV BlockSrc block_src(const PGemmArgs& a, int bx, int blk) {
+  BlockSrc b{0, 0, 0, 0};
+  if constexpr (EPI == PE_QKV) {
+    const int nheads = a.H + 2 * a.Hkv;
+    int head, off;
+    if (a.hd == 128) {
+      head = bx;
+      off = (blk & 1) * 64 + (blk >> 1) * 32;  // blocks 0..3 -> 0, 64, 32, 96
+    } else {
+      head = 2 * bx + (blk >> 1);
+      off = (blk & 1) * 32;
+    }
+    if (head >= nheads) return b;
+    const int vr = head * a.hd + off;
+    const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+    b.vrow0 = vr;
+    b.valid = 32;
+    if (vr >= qrows + krows) { b.mat = 2; b.row0 = vr - qrows - krows; }
+    else if (vr >= qrows) { b.mat = 1; b.row0 = vr - qrows; }
+    else { b.mat = 0; b.row0 = vr; }
+  } else if constexpr (EPI == PE_SWIGLU) {
+    // blocks: gate f0, up f0, gate f0 + 32, up f0 + 32
+    const int f = bx * 64 + (blk >> 1) * 32;
+    b.mat = blk & 1;
+    b.row0 = f;
+    b.valid = f < a.N ? min(32, a.N - f) : 0;
+  } else {
+    const int n = bx * kBM + blk * 32;
+    b.row0 = n;
+    b.valid = n < a.N ? min(32, a.N - n) : 0;
+  }
+  return b;
+}
+
+// One of the three weight matrices, selected arithmetically (an indexed
+// local array would live in scratch memory).
+AIO_DEV const char* pick_mat(const PGemmArgs& a, int mat) {
+  const uint64_t b0 = (uint64_t)a.w0;
+  const uint64_t d1 = (uint64_t)a.w1 - b0, d2 = (uint64_t)a.w2 - b0;
+  return (const char*)(b0 + (uint64_t)(mat == 1) * d1 + (uint64_t)(mat == 2) * d2);
+}
+
+// Global loads of stage st: A_LD 16-byte weight chunks and kBLd activation
+// chunks per thread.
+template <int WFMT, int A_LD>
+AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const (&bptr)[kBLd],
+                         int st, uint4 (&ra)[A_LD], uint4 (&rb)[kBLd]) {
+  constexpr int wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
+  const size_t ko = (size_t)st * kKT;
+#pragma unroll
+  for (int j = 0; j < A_LD; ++j) ra[j] = ld_stream((const uint4*)(aptr[j] + ko * wbytes));
+#pragma unroll
+  for (int j = 0; j < kBLd; ++j) rb[j] = *(const uint4*)(bptr[j] + ko);
+}
+
+// The same chunks into an LDS stage buffer (int8 widened to bf16, exact:
+// |q| <= 127).
+template <int WFMT, int A_LD>
+AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[kBLd],
+                          const uint4 (&ra)[A_LD], const uint4 (&rb)[kBLd]) {
+#pragma unroll
+  for (int j = 0; j < A_LD; ++j) {
+    if constexpr (WFMT == AIO_WFMT_BF16) {
+      *(uint4*)(buf + alds[j]) = ra[j];
+    } else {
+      const uint32_t w[4] = {ra[j].x, ra[j].y, ra[j].z, ra[j].w};
+      uint32_t o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t sw = w[i / 2];
+        const int sh = (i & 1) * 16;
+        const float f0 = (float)(int8_t)(sw >> sh), f1 = (float)(int8_t)(sw >> (sh + 8));
+        o[i] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xffff0000u);
+      }
+      *(uint4*)(buf + alds[j]) = make_uint4(o[0], o[1], o[2], o[3]);
+      *(uint4*)(buf + alds[j] + 16) = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kBLd; ++j) *(uint4*)(buf + blds[j]) = rb[j];
+}
+
+// The MFMA products of one LDS stage: 16-k chunks, the wave's two row blocks
+// by the terms of its 32 prompt rows.  Activation columns of the stage are
+// ordered [wave half wr][term][row].
+AIO_DEV void stage_product(const char* cur, int wn, int wr, int rl, int kh,
+                           f32x16 (&acc)[2][kNT]) {
+#pragma unroll
+  for (int c16 = 0; c16 < kKT / 16; ++c16) {
+    const int koff = (c16 * 16 + 8 * kh) * 2;
+    bf16x8 af[2], bfr[kNT];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      af[b] = as_bf16x8(*(const uint4*)(cur + ((2 * wn + b) * 32 + rl) * kRowB + koff));
+#pragma unroll
+    for (int t = 0; t < kNT; ++t)
+      bfr[t] = as_bf16x8(
+          *(const uint4*)(cur + (kBM + (wr * kNT + t) * 32 + rl) * kRowB + koff));
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < kNT; ++t) acc[b][t] = mfma(af[b], bfr[t], acc[b][t]);
+  }
+}
+
+template <int WFMT, int EPI>
+__global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
+  const int wn = wid & 1, wr = wid >> 1;
+  const int rl = lane & 31, kh = lane >> 5;
+  const int bx = blockIdx.x, r0 = blockIdx.y * kBR;
+  constexpr int wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
+
+  // Staging assignments.  A: row ra of the tile (block ra / 32), 16-byte
+  // chunk ca of the stage's 32 k (bf16: 4 chunks of 8 weights; int8: 2
+  // chunks of 16 weights, widened to 32 bytes in LDS).  B: activation column
+  // cb = (wr' kNT + t) 32 + j -> prompt row r0 + 32 wr' + j, term t; 4
+  // chunks of 8 k.
+  constexpr int A_CPR = WFMT == AIO_WFMT_BF16 ? 4 : 2;
+  constexpr int A_LD = kBM * A_CPR / kGT;
+  const char* aptr[A_LD];
+  int alds[A_LD];
+#pragma unroll
+  for (int j = 0; j < A_LD; ++j) {
+    const int f = j * kGT + tid, ra = f / A_CPR, ca = f % A_CPR;
+    const BlockSrc s = block_src<EPI>(a, bx, ra >> 5);
+    int row = s.row0 + ((ra & 31) < s.valid ? (ra & 31) : 0);
+    if (s.valid == 0) row = 0;  // a block past the end reads row 0 of w0 (discarded)
+    const char* w = s.valid ? pick_mat(a, s.mat) : (const char*)a.w0;
+    aptr[j] = w + ((size_t)row * a.K + (size_t)ca * (16 / wbytes)) * wbytes;
+    alds[j] = ra * kRowB + ca * 16 * (2 / wbytes);
+  }
+  const uint16_t* bptr[kBLd];
+  int blds[kBLd];
+#pragma unroll
+  for (int j = 0; j < kBLd; ++j) {
+    const int f = j * kGT + tid, cb = f / 4, c = f % 4;
+    const int half = cb / (kNT * 32), t = (cb / 32) % kNT;
+    const int row = r0 + half * 32 + (cb & 31);
+    bptr[j] = a.act + t * a.tstride + (size_t)(row < a.R ? row : a.R - 1) * a.lda + c * 8;
+    blds[j] = (kBM + cb) * kRowB + c * 16;
+  }
+  uint4 ra_[A_LD], rb_[kBLd];
+  f32x16 acc[2][kNT];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int t = 0; t < kNT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[b][t][i] = 0.f;
+
+  const int nst = a.K / kKT;
+  gload_stage<WFMT, A_LD>(aptr, bptr, 0, ra_, rb_);
+  lstore_stage<WFMT, A_LD>(smem, alds, blds, ra_, rb_);
+  __syncthreads();
+  // every stage but the last: the next stage's loads are in flight while the
+  // current one is multiplied, then go to the other buffer
+  for (int st = 0; st + 1 < nst; ++st) {
+    gload_stage<WFMT, A_LD>(aptr, bptr, st + 1, ra_, rb_);
+    stage_product(smem + (st & 1) * kStageB, wn, wr, rl, kh, acc);
+    lstore_stage<WFMT, A_LD>(smem + ((st + 1) & 1) * kStageB, alds, blds, ra_, rb_);
+    __syncthreads();
+  }
+  stage_product(smem + ((nst - 1) & 1) * kStageB, wn, wr, rl, kh, acc);
+
+  // Epilogue.  D layout: lane l, register v -> column (prompt row) l % 32,
+  // row i = 8 (v / 4) + 4 (l / 32) + v % 4 of the 32-row block.
+  const int r = r0 + wr * 32 + rl;
+  if (r >= a.R) return;
+  const BlockSrc slo = block_src<EPI>(a, bx, 2 * wn);
+  const BlockSrc shi = block_src<EPI>(a, bx, 2 * wn + 1);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int i = 8 * (v / 4) + 4 * kh + (v % 4);
+    float ylo = acc[0][0][v], yhi = acc[1][0][v];
+#pragma unroll
+    for (int t = 1; t < kNT; ++t) {
+      ylo += acc[0][t][v];
+      yhi += acc[1][t][v];
+    }
+    if constexpr (EPI == PE_QKV) {
+      if (slo.valid == 0) continue;
+      const int half = a.hd / 2;
+      const int vr = slo.vrow0 + i;  // virtual row of the pair's first row
+      const int ii = vr % a.hd;      // its index in the head (< hd / 2)
+      const int mat = slo.mat, row = slo.row0 + i;
+      if constexpr (WFMT == AIO_WFMT_INT8) {
+        const uint16_t* sc = mat == 0 ? a.s0 : (mat == 1 ? a.s1 : a.s2);
+        ylo *= fp16_to_f32(sc[row]);
+        yhi *= fp16_to_f32(sc[row + half]);
+      }
+      const int p = a.pos0 + r;
+      if (mat < 2) {
+        const float2 cs = a.rope[(size_t)p * half + ii];
+        const float r0v = ylo * cs.x - yhi * cs.y;
+        const float r1v = yhi * cs.x + ylo * cs.y;
+        ylo = r0v;
+        yhi = r1v;
+      }
+      if (mat == 0) {
+        a.out[(size_t)r * a.ldo + row] = ylo;
+        a.out[(size_t)r * a.ldo + row + half] = yhi;
+      } else {
+        const int g = row / a.hd;
+        uint16_t* c = (mat == 1 ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
+        c[ii] = f32_to_bf16(ylo);
+        c[ii + half] = f32_to_bf16(yhi);
+      }
+    } else if constexpr (EPI == PE_SWIGLU) {
+      if (i >= slo.valid) continue;
+      const int n = slo.row0 + i;
+      if constexpr (WFMT == AIO_WFMT_INT8) {
+        ylo *= fp16_to_f32(a.s0[n]);
+        yhi *= fp16_to_f32(a.s1[n]);
+      }
+      store_terms(a.act_out + (size_t)r * a.lda_out + n, a.tstride_out,
+                  ylo / (1.f + expf(-ylo)) * yhi);
+    } else {
+      if (i < slo.valid) {
+        const int n = slo.row0 + i;
+        if constexpr (WFMT == AIO_WFMT_INT8) ylo *= fp16_to_f32(a.s0[n]);
+        a.out[(size_t)r * a.ldo + n] += ylo;
+      }
+      if (i < shi.valid) {
+        const int n = shi.row0 + i;
+        if constexpr (WFMT == AIO_WFMT_INT8) yhi *= fp16_to_f32(a.s0[n]);
+        a.out[(size_t)r * a.ldo + n] += yhi;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------ causal attention
+
+struct PAttnArgs {
+  const float* q;       // [R][H hd] rotated queries
+  int ldq;
+  const uint16_t* kc;   // [Hkv][max_ctx][hd]
+  const uint16_t* vc;
+  uint16_t* act;        // [kNT][R][lda]: the output, split, at columns h hd ..
+  int lda;
+  size_t tstride;
+  int R, pos0, H, Hkv, max_ctx;
+  float scale_log2;     // log2(e) / sqrt(hd)
+};
+
+constexpr int kAW = 4;  // waves per workgroup: they split the key blocks
+
+template <int HD>
+struct AttnLds {
+  static constexpr int QROW = HD * 2 + 16;        // bytes per query row of one term
+  static constexpr int QBYTES = 3 * 32 * QROW;     // three terms of 32 queries
+  static constexpr int VROW = 32 * 2 + 16;         // bytes per hd row of a value tile
+  static constexpr int VBYTES = HD * VROW;         // one wave's transposed value tile
+  static constexpr int OBYTES = 2 * 32 * HD * 4 + 2 * 2 * 32 * 4;  // combine: 2 waves' O, m, l
+  static constexpr int TAIL = kAW * VBYTES > OBYTES ? kAW * VBYTES : OBYTES;
+  static constexpr int BYTES = QBYTES + TAIL;
+};
+
+// Position of key kk (0..31 of a block) in a transposed value row.  The
+// softmax weights reach the P V product as the B operand straight from the
+// score tile's registers: lane half kh of chunk c2 holds keys
+// 16 c2 + 4 kh + {0, 1, 2, 3, 8, 9, 10, 11}, so the value rows are stored in
+// that order and the A fragment is one 16-byte read.
+AIO_DEV int vpos(int kk) {
+  const int c2 = kk >> 4, w = kk & 15;
+  return c2 * 16 + ((w >> 2) & 1) * 8 + (w >> 3) * 4 + (w & 3);
+}
+
+// One workgroup per (32 query rows, head): wave w takes key blocks w, w + 4,
+// ... of 32 keys.  Per block: S^T = K Q^T on MFMA (A = 32 key rows from the
+// cache, B = the queries' three bf16 terms from LDS), the online softmax per
+// query (one query per lane pair), then O^T += V^T P^T (A = the transposed
+// value tile, B = the softmax weights' two terms from registers).  The
+// waves' (max, sum, output) states are merged through LDS at the end.
+template <int HD>
+__global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
+  using Lds = AttnLds<HD>;
+  extern __shared__ __align__(16) char smem[];
+  char* qs = smem;                  // [3][32][QROW]
+  char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the merge
+  const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
+  const int rl = lane & 31, kh = lane >> 5;
+  const int q0 = blockIdx.x * 32, h = blockIdx.y;
+  const int G = a.H / a.Hkv, kvh = h / G;
+  const int rows = min(32, a.R - q0);
+  const int n_keys = a.pos0 + q0 + rows;  // keys the block's last row sees
+  const int nkb = (n_keys + 31) / 32;
+
+  // queries, scaled to log2 units and split into three bf16 terms
+  for (int e = tid; e < 32 * HD; e += kAW * AIO_WAVE) {
+    const int qq = e / HD, dim = e % HD;
+    const float v = qq < rows ? a.q[(size_t)(q0 + qq) * a.ldq + (size_t)h * HD + dim] * a.scale_log2
+                              : 0.f;
+    const uint16_t t0 = f32_to_bf16(v);
+    const float r1 = v - bf16_to_f32(t0);
+    const uint16_t t1 = f32_to_bf16(r1);
+    const uint16_t t2 = f32_to_bf16(r1 - bf16_to_f32(t1));
+    *(uint16_t*)(qs + (0 * 32 + qq) * Lds::QROW + dim * 2) = t0;
+    *(uint16_t*)(qs + (1 * 32 + qq) * Lds::QROW + dim * 2) = t1;
+    *(uint16_t*)(qs + (2 * 32 + qq) * Lds::QROW + dim * 2) = t2;
+  }
+  __syncthreads();
+
+  // this lane's query: row q0 + rl sees keys [0, lim]
+  const int lim = a.pos0 + q0 + (rl < rows ? rl : rows - 1);
+  char* vt = tail + wid * Lds::VBYTES;
+  const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD;
+  const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD;
+  constexpr int NHB = HD / 32;
+  f32x16 o[NHB];
+#pragma unroll
+  for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[hb][i] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+
+  for (int kb = wid; kb < nkb; kb += kAW) {
+    const int j0 = kb * 32;
+    // value rows -> LDS, transposed and permuted (16-byte chunks of 8 dims)
+    constexpr int VCH = 32 * HD / 8;
+#pragma unroll
+    for (int it = 0; it < VCH / AIO_WAVE; ++it) {
+      const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
+      const int key = j0 + kk < n_keys ? j0 + kk : 0;
+      const uint4 w = *(const uint4*)(vbase + (size_t)key * HD + d0);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+      char* col = vt + vpos(kk) * 2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        *(uint16_t*)(col + (d0 + 2 * e) * Lds::VROW) = (uint16_t)(ww[e] & 0xffffu);
+        *(uint16_t*)(col + (d0 + 2 * e + 1) * Lds::VROW) = (uint16_t)(ww[e] >> 16);
+      }
+    }
+    // scores: S^T[key i][query j] over the HD dims, three query terms
+    f32x16 s;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[i] = 0.f;
+    {
+      const int key = j0 + rl < n_keys ? j0 + rl : 0;
+      const uint16_t* krow = kbase + (size_t)key * HD;
+#pragma unroll
+      for (int c = 0; c < HD / 16; ++c) {
+        const bf16x8 ak = as_bf16x8(*(const uint4*)(krow + c * 16 + 8 * kh));
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          const bf16x8 bq =
+              as_bf16x8(*(const uint4*)(qs + (t * 32 + rl) * Lds::QROW + (c * 16 + 8 * kh) * 2));
+          s = mfma(ak, bq, s);
+        }
+      }
+    }
+    // causal mask and online softmax for this lane's query (column rl)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int key = j0 + 8 * (v / 4) + 4 * kh + (v % 4);
+      if (key > lim) s[v] = -INFINITY;
+      mx = fmaxf(mx, s[v]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, AIO_WAVE));
+    const float mnew = fmaxf(m, mx);
+    const float c = (m == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : exp2f(m - mnew);
+    float p[16];
+    float ps = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      p[v] = s[v] == -INFINITY ? 0.f : exp2f(s[v] - mnew);
+      ps += p[v];
+    }
+    lsum = lsum * c + ps;
+    m = mnew;
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[hb][i] *= c;
+    wave_lds_sync();  // the value tile is in LDS
+    // O^T += V^T P^T, two chunks of 16 keys, three terms of the weights
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      uint16_t tt[3][8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) split3(p[8 * c2 + e], tt[0][e], tt[1][e], tt[2][e]);
+      bf16x8 bp[3];
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        bp[t] = as_bf16x8(make_uint4(tt[t][0] | ((uint32_t)tt[t][1] << 16),
+                                     tt[t][2] | ((uint32_t)tt[t][3] << 16),
+                                     tt[t][4] | ((uint32_t)tt[t][5] << 16),
+                                     tt[t][6] | ((uint32_t)tt[t][7] << 16)));
+#pragma unroll
+      for (int hb = 0; hb < NHB; ++hb) {
+        const bf16x8 av =
+            as_bf16x8(*(const uint4*)(vt + (hb * 32 + rl) * Lds::VROW + (c2 * 16 + 8 * kh) * 2));
+#pragma unroll
+        for (int t = 0; t < 3; ++t) o[hb] = mfma(av, bp[t], o[hb]);
+      }
+    }
+    wave_lds_sync();  // every read of the value tile is done before the next block's writes
+  }
+  lsum += __shfl_xor(lsum, 32, AIO_WAVE);
+
+  // merge the waves' states: 2, 3 into 0, 1, then 1 into 0
+  __syncthreads();
+  float* om = (float*)tail;                 // [2][32][HD] outputs
+  float* mm = om + 2 * 32 * HD;             // [2][32] max
+  float* ll = mm + 2 * 32;                  // [2][32] sum
+  auto put = [&](int slot) {
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        om[((size_t)slot * 32 + rl) * HD + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
+    if (kh == 0) {
+      mm[slot * 32 + rl] = m;
+      ll[slot * 32 + rl] = lsum;
+    }
+  };
+  auto take = [&](int slot) {
+    const float m2 = mm[slot * 32 + rl], l2 = ll[slot * 32 + rl];
+    const float M = fmaxf(m, m2);
+    const float c1 = m == -INFINITY ? 0.f : exp2f(m - M);
+    const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - M);
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        o[hb][v] = o[hb][v] * c1 +
+                   om[((size_t)slot * 32 + rl) * HD + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] * c2;
+    lsum = lsum * c1 + l2 * c2;
+    m = M;
+  };
+  if (wid >= 2) put(wid - 2);
+  __syncthreads();
+  if (wid < 2) take(wid);
+  __syncthreads();
+  if (wid == 1) put(0);
+  __syncthreads();
+  if (wid != 0) return;
+  take(0);
+  if (rl >= rows) return;
+  const int r = q0 + rl;
+  const float inv = 1.f / lsum;
+  uint16_t* out = a.act + (size_t)r * a.lda + (size_t)h * HD;
+#pragma unroll
+  for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int dim = hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
+      store_terms(out + dim, a.tstride, o[hb][v] * inv);
+    }
+}
+
+// ----------------------------------------------------------------- launchers
+
+hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uint16_t* embed,
+                        const void* gain) {
+  PNormArgs n{};
+  n.x = b.x;
+  n.embed = embed;
+  n.tokens = b.tokens;
+  n.gain = (const uint16_t*)gain;
+  n.act = b.actA;
+  n.lda = b.lda_a;
+  n.tstride = (size_t)b.rcap * b.lda_a;
+  n.d = m.cfg.d_model;
+  n.eps = m.cfg.rms_eps;
+  hipLaunchKernelGGL(k_pnorm, dim3(R), dim3(kNormThreads), 0, m.stream, n);
+  return hipGetLastError();
+}
+
+template <int WFMT, int EPI>
+hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g, int tiles) {
+  const void* fn = (const void*)k_pgemm<WFMT, EPI>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_pgemm<WFMT, EPI>), dim3(tiles, (g.R + kBR - 1) / kBR), dim3(kGT), kGemmLds,
+                     m.stream, g);
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_pgemm(const aio_model& m, const PGemmArgs& g, int tiles) {
+  if (m.cfg.wfmt == AIO_WFMT_INT8) return launch_pgemm_t<AIO_WFMT_INT8, EPI>(m, g, tiles);
+  return launch_pgemm_t<AIO_WFMT_BF16, EPI>(m, g, tiles);
+}
+
+template <int HD>
+hipError_t launch_pattn_t(const aio_model& m, const PAttnArgs& t) {
+  const void* fn = (const void*)k_pattn<HD>;
+  hipError_t e =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, AttnLds<HD>::BYTES);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pattn<HD>, dim3((t.R + 31) / 32, t.H), dim3(kAW * AIO_WAVE),
+                     AttnLds<HD>::BYTES, m.stream, t);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t aio_prefill_row_bytes(const aio_config& c) {
+  const size_t d = (size_t)c.d_model, Hd = (size_t)c.n_heads * c.head_dim, F = (size_t)c.ffn_dim;
+  const size_t ka = d > Hd ? d : Hd;
+  return 4 + 4 * d + 4 * Hd + 2 * kNT * ka + 2 * kNT * F;
+}
+
+PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
+  PfBuffers b{};
+  const size_t d = (size_t)c.d_model, Hd = (size_t)c.n_heads * c.head_dim, F = (size_t)c.ffn_dim;
+  auto al = [](size_t v) { return (v + 255u) & ~(size_t)255u; };
+  size_t off = 0;
+  b.rcap = rcap;
+  b.lda_a = (int)(d > Hd ? d : Hd);
+  b.lda_b = (int)F;
+  b.tokens = (int32_t*)(base + off); off = al(off + 4 * (size_t)rcap);
+  b.x = (float*)(base + off); off = al(off + 4 * d * rcap);
+  b.q = (float*)(base + off); off = al(off + 4 * Hd * rcap);
+  b.actA = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_a * rcap);
+  b.actB = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_b * rcap);
+  b.bytes = off;
+  return b;
+}
+
+// One chunk of R <= b.rcap prompt rows at positions pos0 .. pos0 + R - 1;
+// their tokens are in b.tokens.  On return (enqueued) the cache holds their
+// K/V rows in every layer and b.x row R - 1 the last row's final residual.
+hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int R, int pos0) {
+  const aio_config& c = m.cfg;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const size_t tsA = (size_t)b.rcap * b.lda_a, tsB = (size_t)b.rcap * b.lda_b;
+  hipError_t e;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const aio_layer_weights& L = m.layers[(size_t)l];
+    if ((e = launch_pnorm(m, b, R, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm)) !=
+        hipSuccess)
+      return e;
+
+    PGemmArgs g{};
+    g.act = b.actA; g.lda = b.lda_a; g.tstride = tsA; g.R = R;
+    g.w0 = L.wq; g.w1 = L.wk; g.w2 = L.wv;
+    g.s0 = (const uint16_t*)L.sq; g.s1 = (const uint16_t*)L.sk; g.s2 = (const uint16_t*)L.sv;
+    g.N = (H + 2 * Hkv) * hd; g.K = d;
+    g.out = b.q; g.ldo = H * hd;
+    g.kc = m.kv_layer(l, 0); g.vc = m.kv_layer(l, 1);
+    g.rope = m.rope; g.pos0 = pos0;
+    g.H = H; g.Hkv = Hkv; g.hd = hd; g.max_ctx = c.max_ctx;
+    const int qkv_tiles = hd == 128 ? H + 2 * Hkv : (H + 2 * Hkv + 1) / 2;
+    if ((e = launch_pgemm<PE_QKV>(m, g, qkv_tiles)) != hipSuccess) return e;
+
+    PAttnArgs t{};
+    t.q = b.q; t.ldq = H * hd;
+    t.kc = g.kc; t.vc = g.vc;
+    t.act = b.actA; t.lda = b.lda_a; t.tstride = tsA;
+    t.R = R; t.pos0 = pos0; t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx;
+    t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
+    e = hd == 128 ? launch_pattn_t<128>(m, t) : launch_pattn_t<64>(m, t);
+    if (e != hipSuccess) return e;
+
+    PGemmArgs o{};
+    o.act = b.actA; o.lda = b.lda_a; o.tstride = tsA; o.R = R;
+    o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
+    o.N = d; o.K = H * hd; o.out = b.x; o.ldo = d;
+    if ((e = launch_pgemm<PE_RESID>(m, o, (d + kBM - 1) / kBM)) != hipSuccess) return e;
+
+    if ((e = launch_pnorm(m, b, R, nullptr, L.ffn_norm)) != hipSuccess) return e;
+    PGemmArgs gu{};
+    gu.act = b.actA; gu.lda = b.lda_a; gu.tstride = tsA; gu.R = R;
+    gu.w0 = L.w_gate; gu.w1 = L.w_up;
+    gu.s0 = (const uint16_t*)L.s_gate; gu.s1 = (const uint16_t*)L.s_up;
+    gu.N = F; gu.K = d;
+    gu.act_out = b.actB; gu.lda_out = b.lda_b; gu.tstride_out = tsB;
+    if ((e = launch_pgemm<PE_SWIGLU>(m, gu, (F + 63) / 64)) != hipSuccess) return e;
+
+    PGemmArgs dn{};
+    dn.act = b.actB; dn.lda = b.lda_b; dn.tstride = tsB; dn.R = R;
+    dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
+    dn.N = d; dn.K = F; dn.out = b.x; dn.ldo = d;
+    if ((e = launch_pgemm<PE_RESID>(m, dn, (d + kBM - 1) / kBM)) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}

@@ -783,3 +783,16 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
   lm.N = c.vocab; lm.K = d; lm.out = logits; lm.ldo = c.vocab; lm.st = m.state();
   return launch_vgemm<EPI_STORE>(m, lm, (c.vocab + 63) / 64);
 }
+
+hipError_t aio_launch_lm_rows(const aio_model& m, int rows, float* logits) {
+  const aio_config& c = m.cfg;
+  uint16_t* actA = m.at<uint16_t>(m.lay.act);
+  float* x = m.at<float>(m.lay.x);
+  hipError_t e = launch_vnorm(m, x, nullptr, m.final_norm, actA, rows, 0);
+  if (e != hipSuccess) return e;
+  VGemmArgs lm{};
+  lm.act = actA; lm.lda = m.lay.ka; lm.M = rows;
+  lm.w0 = m.lm_head; lm.s0 = (const uint16_t*)m.s_lm_head;
+  lm.N = c.vocab; lm.K = c.d_model; lm.out = logits; lm.ldo = c.vocab; lm.st = m.state();
+  return launch_vgemm<EPI_STORE>(m, lm, (c.vocab + 63) / 64);
+}
