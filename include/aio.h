@@ -325,6 +325,33 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
  * be allocated. */
 int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, float* logits_dev);
 
+/* Bytes of the device array aio_prefill_noalloc takes its scratch from. */
+#define AIO_PREFILL_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* aio_prefill for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid allocation): the
+ * same operation and kernels, with the scratch taken from a fixed array of
+ * AIO_PREFILL_NOALLOC_SCRATCH_BYTES in the library's device memory instead
+ * of library-allocated memory.  It calls no hipMalloc, hipFree or other
+ * allocating routine.  The prompt goes through in passes of at most
+ * aio_prefill_noalloc_rows(cfg) rows (the array divided by the scratch of
+ * one row: 4 (1 + d + H hd + max(d, H hd) + F) bytes, and at most 2048),
+ * so any n works; results equal aio_prefill's up to rounding (bit-identical
+ * where both take the prompt in one pass).  Every GPU holds one such array
+ * for the whole process, shared by all calls on that GPU: calls that
+ * overlap on one GPU (handles on different streams) race and must be
+ * serialised by the caller.  Nothing in the array needs to start at zero:
+ * each call writes every region before reading it.  Asynchronous like
+ * aio_verify; the tokens are copied from host memory on the model's stream.
+ * Errors as aio_prefill, and AIO_EUNSUPPORTED when one row's scratch
+ * exceeds the array (aio_prefill_noalloc_rows(cfg) == 0). */
+int aio_prefill_noalloc(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos,
+                        float* logits_dev);
+
+/* Rows aio_prefill_noalloc takes per pass for this config (0 for an
+ * invalid config or when one row's scratch exceeds the array). */
+int aio_prefill_noalloc_rows(const aio_config* cfg);
+
 /* The probe's routing decision (Section 3.2 and Section 3.3, "Dynamic
  * Policy Routing and Execution"), pure host: the categories' scores are the
  * probe's logits of the n_categories label tokens (host array).  The

@@ -97,6 +97,8 @@ def lib():
                                        P(aio_pld_stats)]
         L.aio_tune_step.argtypes = [vp, i32, i32, vp, i32]
         L.aio_prefill.argtypes = [vp, vp, i32, i32, vp]
+        L.aio_prefill_noalloc.argtypes = [vp, vp, i32, i32, vp]
+        L.aio_prefill_noalloc_rows.argtypes = [P(aio_config)]
         L.aio_probe_route.argtypes = [vp, i32, i32, i32, i32, ctypes.c_float,
                                       P(ctypes.c_float), P(i32)]
         L.aio_spec_generate.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp,
@@ -402,6 +404,17 @@ class DeviceModel:
         t = np.ascontiguousarray(tokens, dtype=np.int32)
         _check(lib().aio_prefill(self.handle, t.ctypes.data, int(t.size), int(pos), _ptr(logits)),
                "aio_prefill")
+
+    def prefill_noalloc(self, tokens, pos: int, logits: torch.Tensor) -> None:
+        """aio_prefill with the scratch in the library's fixed device array
+        (no device allocation)."""
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        _check(lib().aio_prefill_noalloc(self.handle, t.ctypes.data, int(t.size), int(pos),
+                                         _ptr(logits)), "aio_prefill_noalloc")
+
+    @property
+    def prefill_noalloc_rows(self) -> int:
+        return int(lib().aio_prefill_noalloc_rows(ctypes.byref(self.c)))
 
     def tune(self, token: int, pos: int, logits: torch.Tensor, rounds: int = 4) -> None:
         """Calibrate the persistent kernel's gate/up split (aio_tune_step)."""

@@ -82,6 +82,9 @@ struct aio_model {
   // prefill scratch (aio_prefill), library-owned, grown on demand
   char* pf_scratch;
   int pf_rcap;
+  // device address of the static scratch array on this model's GPU
+  // (aio_prefill_noalloc); not owned
+  char* static_scratch;
   // profiling: when prof_ev is set, every launcher records one event after
   // each kernel it enqueues (aio_profile_step)
   mutable hipEvent_t* prof_ev;

@@ -5,13 +5,40 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
 
 #include "aio_internal.h"
 
+// Scratch of aio_prefill_noalloc: one array per GPU the library runs on,
+// held until the process ends.  In host code `scratch` is only a stand-in
+// for the symbol; its device address on each GPU comes from
+// hipGetSymbolAddress (g_scratch_dev), and only that address is ever used.
+static __device__ __align__(256) char scratch[AIO_PREFILL_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_dev[kMaxDevices];  // device address of `scratch` on each GPU (null until set up)
+
+// The device address of `scratch` on the current device, resolved once per
+// device (with that device current).
+hipError_t scratch_address(int dev, char** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_dev[dev] = (char*)p;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
 
 thread_local int g_last_hip = 0;
 
@@ -191,9 +218,13 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
   if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return hip_fail(e);
   if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return AIO_EUNSUPPORTED;
 
+  char* static_scratch = nullptr;
+  if ((e = scratch_address(dev, &static_scratch)) != hipSuccess) return hip_fail(e);
+
   aio_model* m = new (std::nothrow) aio_model();
   if (!m) return AIO_ENOMEM;
   m->cfg = *cfg;
+  m->static_scratch = static_scratch;
   m->layers.assign(w->layers, w->layers + cfg->n_layers);
   m->embed = w->embed;
   m->final_norm = w->final_norm;
@@ -646,6 +677,27 @@ int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, flo
     m->pf_rcap = want;
   }
   const PfBuffers b = aio_prefill_buffers(m->cfg, m->pf_scratch, m->pf_rcap);
+  const hipError_t e = enqueue_prefill(m, b, tokens, n, pos, logits_dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
+}
+
+int aio_prefill_noalloc_rows(const aio_config* cfg) {
+  if (aio_check_config(cfg) != AIO_OK) return 0;
+  // as many rows as the array holds, padding of the regions included
+  const size_t cap = AIO_PREFILL_NOALLOC_SCRATCH_BYTES;
+  int rcap = (int)std::min<size_t>(cap / aio_prefill_row_bytes(*cfg), (size_t)kPrefillChunk);
+  while (rcap > 0 && aio_prefill_buffers(*cfg, nullptr, rcap).bytes > cap) --rcap;
+  return rcap;
+}
+
+int aio_prefill_noalloc(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos,
+                        float* logits_dev) {
+  int rc = check_prefill(m, tokens, n, pos, logits_dev);
+  if (rc) return rc;
+  if (!m->static_scratch) return AIO_EINVAL;
+  const int rcap = aio_prefill_noalloc_rows(&m->cfg);
+  if (rcap < 1) return AIO_EUNSUPPORTED;  // one row's scratch exceeds the array
+  const PfBuffers b = aio_prefill_buffers(m->cfg, m->static_scratch, rcap);
   const hipError_t e = enqueue_prefill(m, b, tokens, n, pos, logits_dev);
   return e == hipSuccess ? AIO_OK : hip_fail(e);
 }
