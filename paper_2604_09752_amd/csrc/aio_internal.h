@@ -31,6 +31,8 @@ struct WsLayout {
   size_t part_ml;  // fp32 [MV][H][S][2]      split-KV (max, sum) in log2 units
   size_t act;      // bf16 [2][32][KA]        split activations for the verify GEMM
   size_t vpart;    // fp32 [kVerifyMaxKs][MV][d] verify residual products split over K
+  size_t vss;      // fp32 [MV][d/64]         verify rows' sums of squares per 64 columns
+  size_t vcnt;     // int32 [d/64]            arrived K slices per column tile, zeroed at load
   size_t amax;     // int32 [MV]              argmax scratch
   size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters
   // step-kernel exchange buffers (tagged words), mega_xa .. mega_end zeroed at load

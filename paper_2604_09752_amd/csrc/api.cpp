@@ -97,6 +97,8 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * 2 * 4);
   L.act = off; off = align256(off + 2 * 32 * ka * 2);  // two split-activation buffers
   L.vpart = off; off = align256(off + (size_t)kVerifyMaxKs * MV * d * 4);
+  L.vss = off; off = align256(off + MV * (d / 64) * 4);
+  L.vcnt = off; off = align256(off + (d / 64) * 4);
   L.amax = off; off = align256(off + MV * 4);
   L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
   L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
@@ -294,6 +296,7 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
                       hipMemcpyHostToDevice);
     }
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
+    if (e == hipSuccess) e = hipMemset(m->ws + m->lay.vcnt, 0, (size_t)(cfg->d_model / 64) * 4);
     if (e == hipSuccess)
       e = hipMemset(m->ws + m->lay.mega_xa, 0, m->lay.mega_end - m->lay.mega_xa);
   }

@@ -12,10 +12,19 @@
 // convert to bf16 exactly (|q| <= 127) and their fp16 scale is applied in the
 // epilogue.
 //
-// Per layer: vnorm (RMSNorm + split) -> QKV GEMM (+RoPE, K/V append) ->
-// vattn (causal split-KV, row r sees positions [0, pos + r]) -> vmerge
-// (+split) -> O GEMM (+residual) -> vnorm -> gate/up GEMM (+SwiGLU, split)
-// -> down GEMM (+residual); then vnorm -> LM head GEMM -> logits [M][V].
+// RMSNorm is folded into the products around it.  Its scale
+// 1 / sqrt(mean(x_r^2) + eps) is one number per row, so it commutes with the
+// product: the GEMM that consumes a normed row multiplies the split of x * g
+// and scales its result by the row's factor, which it forms from the row's
+// sums of squares over 64-column chunks (written by whoever completed those
+// columns of x, summed in chunk order).
+//
+// Per layer: QKV GEMM (+norm scale, RoPE, K/V append) -> vattn (causal
+// split-KV, row r sees positions [0, pos + r]) -> vmerge (+split) -> O GEMM
+// (+residual, split of x * g_ffn, sums of squares) -> gate/up GEMM (+norm
+// scale, SwiGLU, split) -> down GEMM (+residual, split of x * g for the next
+// layer or the final norm); then the LM head GEMM (+norm scale) -> logits
+// [M][V].  Layer 0's input (the embedding rows) goes through vnorm.
 #include <math.h>
 
 #include "aio_internal.h"
@@ -31,6 +40,37 @@ constexpr int kMaxRows = AIO_MAX_VERIFY_ROWS;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
+
+// 16-byte loads through a global-address-space pointer.  Selected from a
+// table the pointer's address space is unknown, and a flat load also counts
+// against the LDS wait counter: every LDS wait would then wait for the
+// weights in flight as well.
+AIO_DEV uint4 ldg_nt(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load((gl_u32x4*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+AIO_DEV uint4 ldg(const void* p) {
+  const u32x4 v = *(gl_u32x4*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Device-coherent access for the slices of a split residual product: the
+// parts are written through to memory and read past the (per-XCD) L2, so
+// handing them over needs no fence that writes back or drops a whole L2
+// (with fences, the hand-over cost about 40 us per product).
+AIO_DEV int atomic_add_agent(int* p, int v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV void atomic_store_agent(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV float ld_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
 
@@ -56,67 +96,34 @@ AIO_DEV void store_split(uint16_t* act, int lda, int M, int r, int col, float v)
 struct VNormArgs {
   float* x;                 // [M][d] residual rows
   const uint16_t* embed;    // layer 0: embedding table (tokens from state), else null
-  const float* part;        // [nparts][M][d] K-slice products still to add to x, or null
-  int nparts;
   const uint16_t* gain;
-  uint16_t* act;            // [32][lda] split output
+  uint16_t* act;            // [32][lda] split of x * g
   int lda, d, M;
+  float* ss;                // [M][d / 64] sums of squares of x over 64-column chunks
   const aio_state* st;
-  float eps;
 };
 
-// One workgroup of 1024 threads per row r: h = x_r / sqrt(mean(x_r^2) + eps)
-// * g, split.  Each thread keeps up to kNormVals of its elements in
-// registers between the two passes (all of them for d <= 8192).
-//
-// The row x_r is first completed: in layer 0 it is the embedding row of the
-// row's token; after a residual product that was split over K it is x_r plus
-// the slices' products, added in slice order, so the sum (and everything
-// after it) is the same on every run.  The completed row is written back.
+// One workgroup of 1024 threads per row r (in layer 0 x_r is the embedding
+// row of the row's token, written to x): the split of x_r * g and the sums of
+// squares of x_r per 64-column chunk.  Wave w holds chunks w, w + 16, ...
 constexpr int kNormBlock = 1024;
-constexpr int kNormVals = 8;
 
 __global__ __launch_bounds__(kNormBlock) void k_vnorm(VNormArgs a) {
-  __shared__ float red[kNormBlock / AIO_WAVE];
   const int r = blockIdx.x, tid = threadIdx.x;
   const uint16_t* emb = a.embed ? a.embed + (size_t)a.st->token[r] * a.d : nullptr;
   float* xr = a.x + (size_t)r * a.d;
-  const bool write_x = emb || a.nparts > 0;
-  auto val = [&](int e) {
-    if (emb) return bf16_to_f32(emb[e]);
-    float v = xr[e];
-    for (int s = 0; s < a.nparts; ++s) v += a.part[((size_t)s * a.M + r) * a.d + e];
-    return v;
-  };
-  float v[kNormVals];
-  float ss = 0.f;
-#pragma unroll
-  for (int i = 0; i < kNormVals; ++i) {
-    const int e = tid + i * kNormBlock;
-    v[i] = e < a.d ? val(e) : 0.f;
-    ss = fmaf(v[i], v[i], ss);
+  for (int e = tid; e < a.d; e += kNormBlock) {  // wave-uniform: d % 64 == 0
+    float v;
+    if (emb) {
+      v = bf16_to_f32(emb[e]);
+      xr[e] = v;
+    } else {
+      v = xr[e];
+    }
+    store_split(a.act, a.lda, a.M, r, e, v * bf16_to_f32(a.gain[e]));
+    const float sq = wave_sum(v * v);
+    if ((tid & (AIO_WAVE - 1)) == 0) a.ss[(size_t)r * (a.d / 64) + e / 64] = sq;
   }
-  for (int e = tid + kNormVals * kNormBlock; e < a.d; e += kNormBlock) {
-    const float x = val(e);
-    ss = fmaf(x, x, ss);
-  }
-  ss = wave_sum(ss);
-  if ((tid & (AIO_WAVE - 1)) == 0) red[tid / AIO_WAVE] = ss;
-  __syncthreads();
-  float tot = 0.f;
-#pragma unroll
-  for (int w = 0; w < kNormBlock / AIO_WAVE; ++w) tot += red[w];
-  const float inv = rsqrtf(tot / (float)a.d + a.eps);
-  auto out = [&](int e, float x) {
-    if (write_x) xr[e] = x;
-    store_split(a.act, a.lda, a.M, r, e, x * inv * bf16_to_f32(a.gain[e]));
-  };
-#pragma unroll
-  for (int i = 0; i < kNormVals; ++i) {
-    const int e = tid + i * kNormBlock;
-    if (e < a.d) out(e, v[i]);
-  }
-  for (int e = tid + kNormVals * kNormBlock; e < a.d; e += kNormBlock) out(e, val(e));
 }
 
 // ------------------------------------------------------------- skinny GEMM
@@ -142,6 +149,17 @@ struct VGemmArgs {
   int H, Hkv, hd, max_ctx;
   int ks;                   // K splits across workgroups (grid.y); > 1 only for EPI_RESID
   float* part;              // RESID with ks > 1: [ks][M][ldo], slice y's product
+  // QKV, SWIGLU, STORE: the act columns are the split of x * g; each output
+  // is scaled by 1 / sqrt(sum(ss_in[r][0 .. nt)) / K + eps)
+  const float* ss_in;
+  int nt;
+  float eps;
+  // RESID: completes x (ldo == N == d), then writes act_next = split of
+  // x * g_next and ss_out [M][N / 64]; cnt [N / 64] counts arrived slices
+  int* cnt;
+  const uint16_t* g_next;
+  uint16_t* act_next;
+  float* ss_out;
 };
 
 // The k of the two MFMA fragments a lane holds in a block of 32 k (lane
@@ -153,12 +171,14 @@ AIO_DEV int vk_lo(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 8 
 template <int WFMT>
 AIO_DEV int vk_hi(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 16 + 8 * kh : block + 16 * kh + 8; }
 
-// Weights reach the MFMA through LDS in stages of 256 k.  Read straight
-// into the MFMA operand layout, every load instruction would span 32 rows at
-// 16-32 bytes each; staged, one wave instruction reads 512 (bf16) or 256
-// (int8) contiguous bytes of each of 2 or 4 rows, and the 64 rows of a stage
-// go to LDS with a 16-byte skew per row, so that the fragment reads (32 rows
-// at one column) fall in distinct banks.
+// Weights reach the MFMA through LDS in stages of 1 KB per row (512 k of
+// bf16, 1024 k of int8): 64 KB per stage, two stages in flight per
+// workgroup, which is what keeps HBM busy (about 128 KB in flight per CU;
+// with 16-32 KB stages the products streamed at 2-4 TB/s).  Read straight
+// into the MFMA operand layout, every load instruction would span 32 rows
+// at 16-32 bytes each; staged, one wave instruction reads 1 KB of one row,
+// and the 64 rows of a stage go to LDS with a 16-byte skew per row, so that
+// the fragment reads (32 rows at one column) spread over the banks.
 template <int WFMT>
 struct VStage {
   static constexpr int KC = 256;                                     // k per stage
@@ -166,6 +186,8 @@ struct VStage {
   static constexpr int RS = RB + 16;                                 // LDS row stride
   static constexpr int CPR = RB / 16;                                // 16-byte chunks per row
   static constexpr int NLD = 64 * CPR / kGBlock;                     // loads per thread
+  static constexpr int BPS = KC / 32;                                // 32-k blocks per stage
+  static constexpr int BPW = BPS / kGWaves;                          // blocks per wave
   static constexpr int BYTES = 64 * RS;
 };
 
@@ -220,14 +242,25 @@ AIO_DEV void vmma(const VFrag<WFMT, T>& f, bool col_live, f32x16 (&acc)[T]) {
   }
 }
 
+// LDS of a skinny-GEMM workgroup: the weight stage during the product, then
+// the partial tiles of the waves and a residual tile [M][64].
+constexpr int kVRedBytes = (int)sizeof(float) * (kGWaves / 2) * 2 * 32 * 33;
+constexpr int kVFinBytes = (int)sizeof(float) * kMaxRows * 64;
+template <int WFMT>
+constexpr int vgemm_lds() {
+  return VStage<WFMT>::BYTES > kVRedBytes + kVFinBytes ? VStage<WFMT>::BYTES
+                                                       : kVRedBytes + kVFinBytes;
+}
+
 template <int WFMT, int EPI>
 __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   constexpr int T = 2;
   using St = VStage<WFMT>;
-  constexpr int kRedBytes = (int)sizeof(float) * (kGWaves / 2) * T * 32 * 33;
-  // the weight stage during the product, then the partial tiles
-  __shared__ __align__(16) char smem[St::BYTES > kRedBytes ? St::BYTES : kRedBytes];
+  extern __shared__ __align__(16) char smem[];
   float (*red)[T][32][33] = (float (*)[T][32][33])smem;
+  float (*fin)[64] = (float (*)[64])(smem + kVRedBytes);
+  __shared__ float inv_s[kMaxRows];
+  __shared__ int last_s;
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
   const int rl = lane & 31, kh = lane >> 5;
   const size_t wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
@@ -258,15 +291,33 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   }
   const int n_rows_w = (EPI == EPI_QKV) ? 0 : a.N;  // clamp bound for plain tiles
   const bool col_live = rl < 3 * a.M;
+  // Norm scales: wave w sums the chunk sums of rows w and w + 8, lane l
+  // taking chunks l and l + 64 (written by an earlier kernel).  They are
+  // requested here and added only in the epilogue, so no wait in the
+  // product is spent on them.
+  static_assert(kMaxRows <= 2 * kGWaves, "two rows per wave");
+  float ssp[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+  if (EPI != EPI_RESID) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = wid + kGWaves * h;
+      if (r < a.M) {
+        const float* ssr = a.ss_in + (size_t)r * a.nt;
+        if (lane < a.nt) ssp[h][0] = ssr[lane];
+        if (lane + 64 < a.nt) ssp[h][1] = ssr[lane + 64];
+      }
+    }
+  }
   // dead columns read row 0 (in bounds) and are zeroed before the product
   const uint16_t* actp = a.act + (size_t)(col_live ? rl : 0) * a.lda;
 
-  // This workgroup's K slice in stages of 8 blocks of 32 k; wave w
-  // multiplies block w of every stage.
+  // This workgroup's K slice in stages of BPS blocks of 32 k; wave w
+  // multiplies blocks w, w + 8, ... of every stage.
+  constexpr int BPS = St::BPS, BPW = St::BPW;
   const int nkb = a.K / 32;
   const int ks = (int)blockIdx.y;
   const int kbA = ks * nkb / a.ks, kbB = (ks + 1) * nkb / a.ks;
-  const int nst = (kbB - kbA + 7) / 8;
+  const int nst = (kbB - kbA + BPS - 1) / BPS;
   f32x16 acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t)
@@ -287,12 +338,22 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
     lchunk[j] = c;
   }
   const int kend = kbB * 32 * (int)wbytes - 16;  // last 16-byte chunk of the slice
-  auto gload = [&](uint4 (&R)[St::NLD], int st) {
+  // A stage's weight chunks and this wave's activation fragments of it are
+  // requested together, so waiting for one stage never waits for the
+  // other stage's loads (vector loads complete in order); a block past the
+  // slice re-reads the slice's last block and is not multiplied.
+  auto gload = [&](uint4 (&R)[St::NLD], uint4 (&A)[BPW][2], int st) {
 #pragma unroll
     for (int j = 0; j < St::NLD; ++j) {
-      int off = (kbA + st * 8) * 32 * (int)wbytes + lchunk[j] * 16;
+      int off = (kbA + st * BPS) * 32 * (int)wbytes + lchunk[j] * 16;
       off = off < kend ? off : kend;
-      R[j] = ld_stream((const uint4*)(lrow[j] + off));
+      R[j] = ldg_nt(lrow[j] + off);
+    }
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int block = min(kbA + st * BPS + wid + kGWaves * j, kbB - 1);
+      A[j][0] = ldg(actp + vk_lo<WFMT>(block * 32, kh));
+      A[j][1] = ldg(actp + vk_hi<WFMT>(block * 32, kh));
     }
   };
   auto stage = [&](const uint4 (&R)[St::NLD]) {
@@ -301,43 +362,49 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
     for (int j = 0; j < St::NLD; ++j) *(uint4*)(smem + lds_off[j]) = R[j];
     __syncthreads();
   };
-  auto product = [&](int st) {
-    const int block = kbA + st * 8 + wid;
-    if (block < kbB) {
+  // Branch-free: a block past the slice multiplies zeros, so every path
+  // through the loop has the same loads in flight and each wait names only
+  // the stage it needs.
+  auto product = [&](int st, const uint4 (&A)[BPW][2]) {
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int wb = wid + kGWaves * j;
+      const bool live = col_live && kbA + st * BPS + wb < kbB;
       VFrag<WFMT, T> f;
 #pragma unroll
       for (int t = 0; t < T; ++t)
-        frag_lds<WFMT>(smem + (t * 32 + rl) * St::RS, wid, kh, f.wa[t], f.wb[t]);
-      const int b0 = block * 32;
-      f.ba = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + vk_lo<WFMT>(b0, kh)));
-      f.bb = __builtin_bit_cast(bf16x8, *(const uint4*)(actp + vk_hi<WFMT>(b0, kh)));
-      vmma(f, col_live, acc);
+        frag_lds<WFMT>(smem + (t * 32 + rl) * St::RS, wb, kh, f.wa[t], f.wb[t]);
+      f.ba = __builtin_bit_cast(bf16x8, A[j][0]);
+      f.bb = __builtin_bit_cast(bf16x8, A[j][1]);
+      vmma(f, live, acc);
     }
   };
   if (nst > 0) {
-    // two stages in flight in registers; the scheduling barriers keep each
-    // set's refill right after it has gone to LDS
+    // two stages in flight in registers: each set is refilled as soon as
+    // its stage has gone to LDS and been multiplied (the scheduling
+    // barriers keep that order)
     uint4 R0[St::NLD], R1[St::NLD];
-    gload(R0, 0);
-    gload(R1, 1);
+    uint4 A0[BPW][2], A1[BPW][2];
+    gload(R0, A0, 0);
+    gload(R1, A1, 1);
     int st = 0;
     for (; st + 2 < nst; st += 2) {
       stage(R0);
+      product(st, A0);
       __builtin_amdgcn_sched_barrier(0);
-      gload(R0, st + 2);
+      gload(R0, A0, st + 2);
       __builtin_amdgcn_sched_barrier(0);
-      product(st);
       stage(R1);
+      product(st + 1, A1);
       __builtin_amdgcn_sched_barrier(0);
-      gload(R1, st + 3);
+      gload(R1, A1, st + 3);
       __builtin_amdgcn_sched_barrier(0);
-      product(st + 1);
     }
     stage(R0);
-    product(st);
+    product(st, A0);
     if (st + 1 < nst) {
       stage(R1);
-      product(st + 1);
+      product(st + 1, A1);
     }
   }
   __syncthreads();  // the stage buffer becomes the partial-tile buffer
@@ -361,6 +428,18 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
         r += acc[t][v];
       }
   }
+  if (EPI != EPI_RESID) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = wid + kGWaves * h;
+      if (r < a.M) {
+        float p = ssp[h][0] + ssp[h][1];
+        for (int c = lane + 128; c < a.nt; c += 64) p += a.ss_in[(size_t)r * a.nt + c];
+        const float sum = wave_sum(p);
+        if (lane == 0) inv_s[r] = rsqrtf(sum / (float)a.K + a.eps);
+      }
+    }
+  }
   __syncthreads();
 
   // Sum the four wave pairs and the three split terms: y[r][i] for the tile.
@@ -375,7 +454,7 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
 #pragma unroll
       for (int w = 0; w < kGWaves / 2; ++w)
         s += red[w][t][i][r] + red[w][t][i][M + r] + red[w][t][i][2 * M + r];
-      y[t] = s;
+      y[t] = EPI == EPI_RESID ? s : s * inv_s[r];
     }
     if constexpr (EPI == EPI_QKV) {
       const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
@@ -431,13 +510,52 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
         if constexpr (WFMT == AIO_WFMT_INT8) v *= fp16_to_f32(a.s0[n]);
         if constexpr (EPI == EPI_RESID) {
           // K split over workgroups: each slice stores its part of the
-          // product, and the next RMSNorm adds the parts in slice order
-          if (a.ks > 1) a.part[((size_t)blockIdx.y * M + r) * a.ldo + n] = v;
-          else a.out[(size_t)r * a.ldo + n] += v;
+          // product; the slice that arrives last adds them in slice order
+          if (a.ks > 1) st_agent(a.part + ((size_t)blockIdx.y * M + r) * a.ldo + n, v);
+          else fin[r][t * 32 + i] = v;
         } else {
           a.out[(size_t)r * a.ldo + n] = v;
         }
       }
+    }
+  }
+  if constexpr (EPI == EPI_RESID) {
+    if (a.ks > 1) {
+      // every wave's part stores have completed (written through) before
+      // the slice is counted; the last slice to arrive (in whatever order)
+      // then reads the others' parts, which the count shows are in memory
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (tid == 0) last_s = atomic_add_agent(a.cnt + blockIdx.x, 1) == a.ks - 1;
+      __syncthreads();
+      if (!last_s) return;
+      if (tid == 0) atomic_store_agent(a.cnt + blockIdx.x, 0);  // ready for the next product
+    } else {
+      __syncthreads();
+    }
+    // columns c0 .. c0 + 63 of the M rows, one row per wave pass; every
+    // slot is requested before the first is added (slots past ks read
+    // slot 0 and add nothing)
+    const int c0 = blockIdx.x * 64, nt = a.N / 64;
+    for (int e = tid; e < 64 * M; e += kGBlock) {
+      const int r = e / 64, c = e % 64, n = c0 + c;
+      float* xp = a.out + (size_t)r * a.ldo + n;
+      float xn = *xp;
+      if (a.ks > 1) {
+        float pv[kVerifyMaxKs];
+#pragma unroll
+        for (int k = 0; k < kVerifyMaxKs; ++k)
+          pv[k] = ld_agent(a.part + ((size_t)(k < a.ks ? k : 0) * M + r) * a.ldo + n);
+#pragma unroll
+        for (int k = 0; k < kVerifyMaxKs; ++k)
+          if (k < a.ks) xn += pv[k];
+      } else {
+        xn += fin[r][c];
+      }
+      *xp = xn;
+      store_split(a.act_next, a.lda, M, r, n, xn * bf16_to_f32(a.g_next[n]));
+      const float sq = wave_sum(xn * xn);
+      if (lane == 0) a.ss_out[(size_t)r * nt + blockIdx.x] = sq;
     }
   }
 }
@@ -657,44 +775,56 @@ __global__ __launch_bounds__(128) void k_vmerge(VMergeArgs a) {
 // Launch with `blocks` tile pairs.  A residual-add product with fewer tile
 // pairs than CUs also splits K over workgroups, as far as every wave keeps
 // at least two blocks of 32 k (at most kVerifyMaxKs slices); the others run
-// one K slice per workgroup.  *ks_out receives the slice count: with more
-// than one, the slices' products are in the vpart region, still to be added.
+// one K slice per workgroup.  Split slices store their products in the vpart
+// region and count themselves in vcnt.
 template <int EPI>
-hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks, int* ks_out = nullptr) {
+hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
   VGemmArgs a = g;
   a.ks = 1;
+  a.nt = m.cfg.d_model / 64;
+  a.eps = m.cfg.rms_eps;
   if (EPI == EPI_RESID) {
     const int nkb = a.K / 32;
     while (blocks * a.ks < m.num_cus && 2 * a.ks <= kVerifyMaxKs &&
            nkb / (2 * a.ks * kGWaves) >= 2)
       a.ks *= 2;
     a.part = m.at<float>(m.lay.vpart);
+    a.cnt = m.at<int>(m.lay.vcnt);
+    a.ss_out = m.at<float>(m.lay.vss);
+  } else {
+    a.ss_in = m.at<float>(m.lay.vss);
   }
-  if (ks_out) *ks_out = a.ks;
   const dim3 grid(blocks, a.ks);
-  if (m.cfg.wfmt == AIO_WFMT_INT8)
-    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), grid, dim3(kGBlock), 0, m.stream, a);
-  else
-    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), grid, dim3(kGBlock), 0, m.stream, a);
+  if (m.cfg.wfmt == AIO_WFMT_INT8) {
+    constexpr int lds = vgemm_lds<AIO_WFMT_INT8>();
+    const hipError_t e = hipFuncSetAttribute((const void*)k_vgemm<AIO_WFMT_INT8, EPI>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_INT8, EPI>), grid, dim3(kGBlock), lds, m.stream, a);
+  } else {
+    constexpr int lds = vgemm_lds<AIO_WFMT_BF16>();
+    const hipError_t e = hipFuncSetAttribute((const void*)k_vgemm<AIO_WFMT_BF16, EPI>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), grid, dim3(kGBlock), lds, m.stream, a);
+  }
   return hipGetLastError();
 }
 
-// RMSNorm of the M rows of x; `nparts` K-slice products (vpart) are first
-// added to x (launch_vgemm's slice count, or 0).
+// Split of x * g and chunk sums of squares for the M rows of x (layer 0:
+// x is first set to the embedding rows).
 hipError_t launch_vnorm(const aio_model& m, float* x, const uint16_t* embed, const void* gain,
-                        uint16_t* act, int M, int nparts) {
+                        uint16_t* act, int M) {
   VNormArgs n{};
   n.x = x;
   n.embed = embed;
-  n.part = m.at<float>(m.lay.vpart);
-  n.nparts = nparts > 1 ? nparts : 0;
   n.gain = (const uint16_t*)gain;
   n.act = act;
   n.lda = m.lay.ka;
   n.d = m.cfg.d_model;
   n.M = M;
+  n.ss = m.at<float>(m.lay.vss);
   n.st = m.state();
-  n.eps = m.cfg.rms_eps;
   hipLaunchKernelGGL(k_vnorm, dim3(M), dim3(kNormBlock), 0, m.stream, n);
   return hipGetLastError();
 }
@@ -711,13 +841,11 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
   uint16_t* actB = actA + (size_t)32 * ka;
   float* x = m.at<float>(m.lay.x);
   float* q = m.at<float>(m.lay.q);
-  hipError_t e;
-  int pend = 0;  // K slices of the last residual product not yet added to x
+  hipError_t e = launch_vnorm(m, x, (const uint16_t*)m.embed, m.layers[0].attn_norm, actA, M);
+  if (e != hipSuccess) return e;
   for (int l = 0; l < c.n_layers; ++l) {
     const aio_layer_weights& L = m.layers[(size_t)l];
-    e = launch_vnorm(m, x, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm, actA, M,
-                     pend);
-    if (e != hipSuccess) return e;
+    const void* g_after = l + 1 < c.n_layers ? m.layers[(size_t)l + 1].attn_norm : m.final_norm;
 
     VGemmArgs g{};
     g.act = actA; g.lda = ka; g.M = M;
@@ -760,9 +888,9 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     o.act = actB; o.lda = ka; o.M = M;
     o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
     o.N = d; o.K = H * hd; o.out = x; o.ldo = d; o.st = m.state();
-    if ((e = launch_vgemm<EPI_RESID>(m, o, (d + 63) / 64, &pend)) != hipSuccess) return e;
+    o.g_next = (const uint16_t*)L.ffn_norm; o.act_next = actA;
+    if ((e = launch_vgemm<EPI_RESID>(m, o, d / 64)) != hipSuccess) return e;
 
-    if ((e = launch_vnorm(m, x, nullptr, L.ffn_norm, actA, M, pend)) != hipSuccess) return e;
     VGemmArgs gu{};
     gu.act = actA; gu.lda = ka; gu.M = M;
     gu.w0 = L.w_gate; gu.w1 = L.w_up;
@@ -774,9 +902,9 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     dn.act = actB; dn.lda = ka; dn.M = M;
     dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
     dn.N = d; dn.K = F; dn.out = x; dn.ldo = d; dn.st = m.state();
-    if ((e = launch_vgemm<EPI_RESID>(m, dn, (d + 63) / 64, &pend)) != hipSuccess) return e;
+    dn.g_next = (const uint16_t*)g_after; dn.act_next = actA;
+    if ((e = launch_vgemm<EPI_RESID>(m, dn, d / 64)) != hipSuccess) return e;
   }
-  if ((e = launch_vnorm(m, x, nullptr, m.final_norm, actA, M, pend)) != hipSuccess) return e;
   VGemmArgs lm{};
   lm.act = actA; lm.lda = ka; lm.M = M;
   lm.w0 = m.lm_head; lm.s0 = (const uint16_t*)m.s_lm_head;
@@ -788,7 +916,7 @@ hipError_t aio_launch_lm_rows(const aio_model& m, int rows, float* logits) {
   const aio_config& c = m.cfg;
   uint16_t* actA = m.at<uint16_t>(m.lay.act);
   float* x = m.at<float>(m.lay.x);
-  hipError_t e = launch_vnorm(m, x, nullptr, m.final_norm, actA, rows, 0);
+  hipError_t e = launch_vnorm(m, x, nullptr, m.final_norm, actA, rows);
   if (e != hipSuccess) return e;
   VGemmArgs lm{};
   lm.act = actA; lm.lda = m.lay.ka; lm.M = rows;
