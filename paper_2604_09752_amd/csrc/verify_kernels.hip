@@ -171,14 +171,14 @@ AIO_DEV int vk_lo(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 8 
 template <int WFMT>
 AIO_DEV int vk_hi(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 16 + 8 * kh : block + 16 * kh + 8; }
 
-// Weights reach the MFMA through LDS in stages of 1 KB per row (512 k of
-// bf16, 1024 k of int8): 64 KB per stage, two stages in flight per
-// workgroup, which is what keeps HBM busy (about 128 KB in flight per CU;
-// with 16-32 KB stages the products streamed at 2-4 TB/s).  Read straight
-// into the MFMA operand layout, every load instruction would span 32 rows
-// at 16-32 bytes each; staged, one wave instruction reads 1 KB of one row,
-// and the 64 rows of a stage go to LDS with a 16-byte skew per row, so that
-// the fragment reads (32 rows at one column) spread over the banks.
+// Weights reach the MFMA through LDS in stages of 256 k per row (64 rows:
+// 32 KB of bf16, 16 KB of int8), two stages in flight per workgroup.  Read
+// straight into the MFMA operand layout, every load instruction would span
+// 32 rows at 16-32 bytes each; staged, consecutive lanes read consecutive
+// 16-byte chunks of one row, and the 64 rows of a stage go to LDS with a
+// 16-byte skew per row, so that the fragment reads (32 rows at one column)
+// spread over the banks.  Stages of 1 KB per row (64 KB, one workgroup per
+// CU) measured slower: 5.16 against 4.89 ms per 7B bf16 verify.
 template <int WFMT>
 struct VStage {
   static constexpr int KC = 256;                                     // k per stage
