@@ -33,6 +33,7 @@ struct WsLayout {
   size_t vpart;    // fp32 [kVerifyMaxKs][MV][d] verify residual products split over K
   size_t vss;      // fp32 [MV][d/64]         verify rows' sums of squares per 64 columns
   size_t vcnt;     // int32 [d/64]            arrived K slices per column tile, zeroed at load
+  size_t vacnt;    // int32 [H]               finished attention splits per head, zeroed at load
   size_t amax;     // int32 [MV]              argmax scratch
   size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters
   // step-kernel exchange buffers (tagged words), mega_xa .. mega_end zeroed at load
@@ -46,6 +47,7 @@ struct WsLayout {
   size_t mega_end;
   size_t total;
   int splits;      // S, split-KV partitions per head
+  int vsplits;     // most split-KV partitions of a verify attention (part_o holds max(S, this))
   int mega_splits; // S_mega, split-KV partitions per kv head in the step kernel
   int ka;          // KA = max(d, H*hd, F)
 };
@@ -117,7 +119,7 @@ hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, 
                              int32_t* out, bool greedy_feedback);
 
 // ---- launchers (verify_kernels.hip) ----
-hipError_t aio_launch_verify(const aio_model& m, int rows, float* logits);
+hipError_t aio_launch_verify(const aio_model& m, int rows, int pos, float* logits);
 // Final RMSNorm and LM head of the first `rows` rows of the workspace's
 // residual rows (lay.x): logits [rows][vocab].
 hipError_t aio_launch_lm_rows(const aio_model& m, int rows, float* logits);

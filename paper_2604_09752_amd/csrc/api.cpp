@@ -84,6 +84,9 @@ WsLayout aio_ws_layout(const aio_config& c) {
   const size_t MV = (size_t)c.max_verify, d = (size_t)c.d_model, F = (size_t)c.ffn_dim;
   const size_t Hd = (size_t)c.n_heads * (size_t)c.head_dim;
   L.splits = choose_splits(c);
+  // verify attention: at least 4 key blocks of 32 per split, at most 64 splits
+  L.vsplits = (int)std::min<size_t>(64, std::max<size_t>(1, ((size_t)c.max_ctx + 127) / 128));
+  const size_t SP = (size_t)std::max(L.splits, L.vsplits);
   size_t ka = d > Hd ? d : Hd;
   if (F > ka) ka = F;
   L.ka = (int)ka;
@@ -93,12 +96,13 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.q = off; off = align256(off + MV * Hd * 4);
   L.o = off; off = align256(off + MV * Hd * 4);
   L.m = off; off = align256(off + F * 4);
-  L.part_o = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * c.head_dim * 4);
-  L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * (size_t)L.splits * 2 * 4);
+  L.part_o = off; off = align256(off + MV * (size_t)c.n_heads * SP * c.head_dim * 4);
+  L.part_ml = off; off = align256(off + MV * (size_t)c.n_heads * SP * 2 * 4);
   L.act = off; off = align256(off + 2 * 32 * ka * 2);  // two split-activation buffers
   L.vpart = off; off = align256(off + (size_t)kVerifyMaxKs * MV * d * 4);
   L.vss = off; off = align256(off + MV * (d / 64) * 4);
   L.vcnt = off; off = align256(off + (d / 64) * 4);
+  L.vacnt = off; off = align256(off + (size_t)c.n_heads * 4);
   L.amax = off; off = align256(off + MV * 4);
   L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
   L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
@@ -297,6 +301,7 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
     }
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.vcnt, 0, (size_t)(cfg->d_model / 64) * 4);
+    if (e == hipSuccess) e = hipMemset(m->ws + m->lay.vacnt, 0, (size_t)cfg->n_heads * 4);
     if (e == hipSuccess)
       e = hipMemset(m->ws + m->lay.mega_xa, 0, m->lay.mega_end - m->lay.mega_xa);
   }
@@ -352,7 +357,7 @@ int aio_verify(aio_model* m, int32_t token, const int32_t* drafts, int32_t k, in
   rows[0] = token;
   for (int i = 0; i < k; ++i) rows[i + 1] = drafts[i];
   hipError_t e = aio_launch_set_rows(*m, rows, k + 1, pos);
-  if (e == hipSuccess) e = aio_launch_verify(*m, k + 1, logits_dev);
+  if (e == hipSuccess) e = aio_launch_verify(*m, k + 1, pos, logits_dev);
   return e == hipSuccess ? AIO_OK : hip_fail(e);
 }
 

@@ -19,13 +19,15 @@
 // sums of squares over 64-column chunks (written by whoever completed those
 // columns of x, summed in chunk order).
 //
-// Per layer: QKV GEMM (+norm scale, RoPE, K/V append) -> vattn (causal
-// split-KV, row r sees positions [0, pos + r]) -> vmerge (+split) -> O GEMM
+// Per layer: QKV GEMM (+norm scale, RoPE, K/V append) -> vattn_mma (causal
+// split-KV on MFMA, row r sees positions [0, pos + r]; the last split of a
+// head merges the head's splits and writes the split output) -> O GEMM
 // (+residual, split of x * g_ffn, sums of squares) -> gate/up GEMM (+norm
 // scale, SwiGLU, split) -> down GEMM (+residual, split of x * g for the next
 // layer or the final norm); then the LM head GEMM (+norm scale) -> logits
 // [M][V].  Layer 0's input (the embedding rows) goes through vnorm.
 #include <math.h>
+#include <algorithm>
 
 #include "aio_internal.h"
 #include "common.h"
@@ -571,205 +573,363 @@ struct VAttnArgs {
   const aio_state* st;
   int H, Hkv, max_ctx, S, M;
   float scale_log2;
+  // k_vattn_mma: the last split of head h to finish merges the head's
+  // splits into act (split o [32][lda]); cnt [H] counts finished splits
+  int* cnt;
+  uint16_t* act;
+  int lda;
 };
 
-// The verify rows are cut into groups of RG; each row group has its own
-// kAttnWaves waves over the same keys, so a wave holds the state of RG rows
-// only.  A lane group takes KB keys at a time, with the next KB requested
-// before the current ones are scored when PF is set.  Two shapes:
-//   RG 3, KB 2     four row groups, 122 VGPRs, four waves per SIMD: best
-//                  where the keys are few (2K: 5.12 against 5.20 ms per 7B
-//                  verify);
-//   RG 5, KB 4, PF two row groups, 226 VGPRs: each key is read by fewer
-//                  row groups, which wins where the keys are many (32K:
-//                  11.1 against 11.7 ms).
-constexpr int kAttnWaves = 4;
-template <int RG>
-constexpr int attn_block() { return (kMaxRows + RG - 1) / RG * kAttnWaves * AIO_WAVE; }
-static_assert(attn_block<3>() <= 1024, "verify attention workgroup too large");
+// Causal attention of the M verify rows on MFMA.  One workgroup of kVAW
+// waves per (split s, query head h); the split takes key blocks [kbA, kbB)
+// of 32 keys, and wave w the blocks kbA + w, kbA + w + kVAW, ...  Per block:
+//   S^T = K Q^T: A = 32 key rows straight from the cache (exact bf16), B =
+//     the M queries' three bf16 terms (log2-scaled) from LDS; lanes past M
+//     multiply zeros.  The three terms accumulate into one tile, so column r
+//     of S^T is row r's scores in fp32-level precision.
+//   online softmax per query column (causal mask j <= pos + r);
+//   O^T += V^T P^T: A = the value tile (staged in LDS row by row, read back
+//     one bf16 per key and dimension, in the order the score registers hold
+//     the keys), B = the softmax weights' three bf16 terms straight from
+//     registers.  (Transposing on the way in, with one 16-bit store per
+//     element, put 16 lanes on one bank and tripled the kernel's time.)
+// The next block's keys and values are requested before the current one is
+// multiplied.  The waves' (max, sum, output) states merge through LDS; the
+// split's unnormalized state goes to part_o / part_ml, and the head's last
+// split to finish merges all of them (vattn_merge).
+//
+// Four blocks per wave and split measured best at 2K context: 3.20 ms per
+// int8 7B verify against 3.26 with two and 3.50 with one (more splits cost
+// more merging); at 32K the 64-split cap gives each wave 4 blocks as well.
+constexpr int kVAW = 4;
+constexpr int kVattnBlocksPerSplit = 4 * kVAW;
 
-// One workgroup per (split s, query head h).  Keys [0, pos + M - 1] are cut
-// into S splits; row r only takes keys j <= pos + r.
-template <int HD, int RG, int KB, bool PF>
-__global__ __launch_bounds__(attn_block<RG>()) void k_vattn(VAttnArgs a) {
-  constexpr int kAttnRG = RG, kAttnBlock = attn_block<RG>();
-  constexpr int LPK = HD / 8, RGT = kAttnWaves * AIO_WAVE, NG = RGT / LPK;
-  __shared__ float sm_m[kAttnWaves][kMaxRows], sm_l[kAttnWaves][kMaxRows];
-  __shared__ float sm_o[kAttnWaves][kMaxRows][HD];
-  const int tid = threadIdx.x, rt = tid % RGT, r0 = (tid / RGT) * kAttnRG;
-  const int gi = rt / LPK, li = rt % LPK;
-  const int s = blockIdx.x, h = blockIdx.y, G = a.H / a.Hkv, kvh = h / G;
-  const int pos = a.st->pos, M = a.M;
-  const int n_keys = pos + M;
-  const int chunk = (n_keys + a.S - 1) / a.S;
-  const int j0 = s * chunk, j1 = min(n_keys, j0 + chunk);
-  const size_t Hd = (size_t)a.H * HD;
+template <int HD>
+struct VAttnLds {
+  static constexpr int QROW = HD * 2 + 16;                 // bytes per query row of one term
+  static constexpr int QR = kMaxRows + 1;                   // query rows per term (+ a zero row)
+  static constexpr int QBYTES = 3 * QR * QROW;              // three terms of the M queries
+  static constexpr int VROW = HD * 2 + 16;                  // bytes per key row of a value tile
+  static constexpr int VBYTES = 32 * VROW;                  // one wave's value tile
+  static constexpr int OROW = HD + 1;                       // floats per merged output row
+  static constexpr int OBYTES = 2 * 32 * OROW * 4 + 2 * 2 * 32 * 4;  // merge: 2 waves' O, m, l
+  static constexpr int TAIL = kVAW * VBYTES > OBYTES ? kVAW * VBYTES : OBYTES;
+  static constexpr int BYTES = QBYTES + TAIL;
+};
 
-  float q[kAttnRG][8], o[kAttnRG][8], m[kAttnRG], l[kAttnRG];
+// Key of element e (0..7) of lane half kh's softmax weights in 16-key chunk
+// c2: score register v = 8 c2 + e holds key 8 (v / 4) + 4 kh + v % 4.
+AIO_DEV int vattn_key(int c2, int kh, int e) { return 16 * c2 + 8 * (e >> 2) + 4 * kh + (e & 3); }
+
+AIO_DEV bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+// Wait for this wave's LDS operations (also a compiler barrier for LDS).
+AIO_DEV void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Block kb's key fragments (A operand: key row rl, dims 16 c + 8 kh ..) and
+// value chunks (16 bytes each, row-major); keys past n_keys read key 0.
+template <int HD>
+AIO_DEV void vattn_load(const uint16_t* kbase, const uint16_t* vbase, int kb, int n_keys,
+                        int lane, uint4 (&kr)[HD / 16], uint4 (&vr)[32 * HD / 8 / AIO_WAVE]) {
+  const int rl = lane & 31, kh = lane >> 5, j0 = kb * 32;
+  const int key = j0 + rl < n_keys ? j0 + rl : 0;
+  const uint16_t* krow = kbase + (size_t)key * HD;
 #pragma unroll
-  for (int r = 0; r < kAttnRG; ++r) {
-    m[r] = -INFINITY;
-    l[r] = 0.f;
+  for (int c = 0; c < HD / 16; ++c) kr[c] = *(const uint4*)(krow + c * 16 + 8 * kh);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      q[r][i] = r0 + r < M ? a.q[(r0 + r) * Hd + (size_t)h * HD + li * 8 + i] * a.scale_log2 : 0.f;
-      o[r][i] = 0.f;
-    }
-  }
-  const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD + li * 8;
-  const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD + li * 8;
-  // a group requests its KB keys before scoring any (a key past the split
-  // reads the split's first row and is masked)
-  auto fetch = [&](int j, uint4 (&kk)[KB], uint4 (&vv)[KB]) {
-#pragma unroll
-    for (int u = 0; u < KB; ++u) {
-      const int jj = j + u * NG;
-      const size_t off = (size_t)(jj < j1 ? jj : j0) * HD;
-      kk[u] = *(const uint4*)(kbase + off);
-      vv[u] = *(const uint4*)(vbase + off);
-    }
-  };
-  uint4 kk[KB], vv[KB];
-  int j = j0 + gi;
-  const bool rows_here = r0 < M;
-  if (PF && rows_here && j < j1) fetch(j, kk, vv);
-  for (; rows_here && j < j1; j += KB * NG) {
-    uint4 nk[KB], nv[KB];
-    if constexpr (PF) {
-      if (j + KB * NG < j1) fetch(j + KB * NG, nk, nv);
-    } else {
-      fetch(j, kk, vv);
-    }
-#pragma unroll
-    for (int r = 0; r < kAttnRG; ++r) {
-      if (r0 + r < M) {
-        // the scores, each summed over the group's lanes
-        float sc[KB];
-        float mn = m[r];
-#pragma unroll
-        for (int u = 0; u < KB; ++u) {
-          const int jj = j + u * NG;
-          sc[u] = group_sum_dpp<LPK>(
-              dot8_bf16(kk[u], make_float4(q[r][0], q[r][1], q[r][2], q[r][3]),
-                        make_float4(q[r][4], q[r][5], q[r][6], q[r][7]), 0.f));
-          // causal: row r0 + r sees keys [0, pos + r0 + r]
-          if (!(jj < j1 && jj <= pos + r0 + r)) sc[u] = -INFINITY;
-          mn = fmaxf(mn, sc[u]);
-        }
-        // one rescale of the state per batch of keys
-        const float c = mn == -INFINITY ? 1.f : exp2f(m[r] - mn);
-        float p[KB];
-        float ps = 0.f;
-#pragma unroll
-        for (int u = 0; u < KB; ++u) {
-          p[u] = sc[u] == -INFINITY ? 0.f : exp2f(sc[u] - mn);
-          ps += p[u];
-        }
-        l[r] = l[r] * c + ps;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[r][i] *= c;
-#pragma unroll
-        for (int u = 0; u < KB; ++u) {
-          const uint32_t w[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            o[r][2 * i] = fmaf(p[u], bf16_lo(w[i]), o[r][2 * i]);
-            o[r][2 * i + 1] = fmaf(p[u], bf16_hi(w[i]), o[r][2 * i + 1]);
-          }
-        }
-        m[r] = mn;
-      }
-    }
-    if constexpr (PF) {
-#pragma unroll
-      for (int u = 0; u < KB; ++u) {
-        kk[u] = nk[u];
-        vv[u] = nv[u];
-      }
-    }
-  }
-  // combine the groups: first the NG / kAttnWaves groups of each wave with
-  // lane exchanges (every group of the wave ends with the wave's state), then
-  // the kAttnWaves wave states of each row group through LDS
-#pragma unroll
-  for (int off = LPK; off < AIO_WAVE; off <<= 1) {
-#pragma unroll
-    for (int r = 0; r < kAttnRG; ++r) {
-      if (r0 + r >= M) continue;
-      const float m2 = __shfl_xor(m[r], off, AIO_WAVE);
-      const float l2 = __shfl_xor(l[r], off, AIO_WAVE);
-      const float mx = fmaxf(m[r], m2);
-      const float c1 = m[r] == -INFINITY ? 0.f : exp2f(m[r] - mx);
-      const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - mx);
-      l[r] = l[r] * c1 + l2 * c2;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[r][i] = o[r][i] * c1 + __shfl_xor(o[r][i], off, AIO_WAVE) * c2;
-      m[r] = mx;
-    }
-  }
-  const int wv = rt / AIO_WAVE;
-  if (rt % AIO_WAVE < LPK) {  // group 0 of each wave writes the wave's state
-#pragma unroll
-    for (int r = 0; r < kAttnRG; ++r) {
-      const int R = r0 + r;
-      if (R >= M) continue;
-      if (li == 0) {
-        sm_m[wv][R] = m[r];
-        sm_l[wv][R] = l[r];
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) sm_o[wv][R][li * 8 + i] = o[r][i];
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < M * HD; e += kAttnBlock) {
-    const int r = e / HD, dim = e % HD;
-    float Mx = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) Mx = fmaxf(Mx, sm_m[w][r]);
-    float L = 0.f, O = 0.f;
-    if (Mx != -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < kAttnWaves; ++w) {
-        const float mk = sm_m[w][r];
-        const float wt = mk == -INFINITY ? 0.f : exp2f(mk - Mx);
-        L = fmaf(wt, sm_l[w][r], L);
-        O = fmaf(wt, sm_o[w][r][dim], O);
-      }
-    }
-    const size_t slot = ((size_t)r * a.H + h) * a.S + s;
-    a.part_o[slot * HD + dim] = O;
-    if (dim == 0) {
-      a.part_ml[slot * 2] = Mx;
-      a.part_ml[slot * 2 + 1] = L;
-    }
+  for (int it = 0; it < 32 * HD / 8 / AIO_WAVE; ++it) {
+    const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
+    const int vkey = j0 + kk < n_keys ? j0 + kk : 0;
+    vr[it] = *(const uint4*)(vbase + (size_t)vkey * HD + d0);
   }
 }
 
-struct VMergeArgs {
-  const float* part_o;
-  const float* part_ml;
-  uint16_t* act;  // split o [32][lda]
-  int lda, S, hd, H, M;
-};
-
-__global__ __launch_bounds__(128) void k_vmerge(VMergeArgs a) {
-  const int h = blockIdx.x, r = blockIdx.y;
-  const size_t base = ((size_t)r * a.H + h) * a.S;
-  const float* ml = a.part_ml + base * 2;
-  float Mx = -INFINITY;
-  for (int s = 0; s < a.S; ++s) Mx = fmaxf(Mx, ml[2 * s]);
-  for (int dim = threadIdx.x; dim < a.hd; dim += blockDim.x) {
-    float L = 0.f, O = 0.f;
-    for (int s = 0; s < a.S; ++s) {
-      const float ms = ml[2 * s];
-      if (ms == -INFINITY) continue;
-      const float w = exp2f(ms - Mx);
-      L = fmaf(w, ml[2 * s + 1], L);
-      O = fmaf(w, a.part_o[(base + s) * a.hd + dim], O);
+// Merge of head h's S splits for the M rows (by the split that finished
+// last; the others' states are in memory, read past the caches):
+// o_r = sum_s w_rs o_rs with w_rs = 2^(m_rs - max_s m_rs) / L_r and
+// L_r = sum_s 2^(m_rs - max) l_rs, in split order; o_r is split into act.
+// `ws` is LDS for 3 M S + ... floats (the weights, padded to 8 splits).
+template <int HD>
+AIO_DEV void vattn_merge(const VAttnArgs& a, int h, float* ws) {
+  constexpr int NT = kVAW * AIO_WAVE;
+  const int tid = threadIdx.x, M = a.M, S = a.S;
+  const int S8 = (S + 7) & ~7;
+  float* mS = ws;            // [M][S8]
+  float* lS = mS + M * S8;   // [M][S8]
+  float* w = lS + M * S8;    // [M][S8] merge weights, 0 past S
+  for (int t = tid; t < M * S8; t += NT) {
+    const int r = t / S8, sp = t % S8;
+    float mv = -INFINITY, lv = 0.f;
+    if (sp < S) {
+      const float* ml = a.part_ml + (((size_t)r * a.H + h) * S + sp) * 2;
+      mv = ld_agent(ml);
+      lv = ld_agent(ml + 1);
     }
-    store_split(a.act, a.lda, a.M, r, h * a.hd + dim, O / L);
+    mS[t] = mv;
+    lS[t] = lv;
   }
+  __syncthreads();
+  if (tid < M) {
+    float mx = -INFINITY;
+    for (int sp = 0; sp < S; ++sp) mx = fmaxf(mx, mS[tid * S8 + sp]);
+    float L = 0.f;
+    for (int sp = 0; sp < S; ++sp) {
+      const float ms = mS[tid * S8 + sp];
+      if (ms != -INFINITY) L = fmaf(exp2f(ms - mx), lS[tid * S8 + sp], L);
+    }
+    for (int sp = 0; sp < S8; ++sp) {
+      const float ms = mS[tid * S8 + sp];
+      w[tid * S8 + sp] = ms == -INFINITY ? 0.f : exp2f(ms - mx) / L;
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < M * HD; e += NT) {
+    const int r = e / HD, dim = e % HD;
+    const float* po = a.part_o + ((size_t)r * a.H + h) * S * HD + dim;
+    const float* wr = w + r * S8;
+    float o = 0.f;
+    for (int s0 = 0; s0 < S8; s0 += 8) {
+      // eight splits' values requested together (past S: split 0, weight 0)
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = ld_agent(po + (size_t)(s0 + j < S ? s0 + j : 0) * HD);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o = fmaf(wr[s0 + j], v[j], o);
+    }
+    store_split(a.act, a.lda, M, r, h * HD + dim, o);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(kVAW * AIO_WAVE, 2) void k_vattn_mma(VAttnArgs a) {
+  using Lds = VAttnLds<HD>;
+  extern __shared__ __align__(16) char smem[];
+  char* qs = smem;                  // [3][QR][QROW]; row kMaxRows of each term is zero
+  char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the merge
+  const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
+  const int rl = lane & 31, kh = lane >> 5;
+  const int s = blockIdx.x, h = blockIdx.y, M = a.M;
+  const int kvh = h / (a.H / a.Hkv);
+  const int pos = a.st->pos;
+  const int n_keys = pos + M;  // the last row sees keys [0, pos + M - 1]
+  const int nkb = (n_keys + 31) / 32;
+  const int kbA = (int)((long long)s * nkb / a.S), kbB = (int)((long long)(s + 1) * nkb / a.S);
+
+  const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD;
+  const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD;
+  constexpr int NHB = HD / 32;           // 32-dim blocks of the output
+  constexpr int NKC = HD / 16;           // 16-dim chunks of a key row (per lane half)
+  constexpr int NVL = 32 * HD / 8 / AIO_WAVE;  // 16-byte value chunks per lane
+  // The queries are requested first, then the wave's first key block:
+  // loads complete in order, so waiting for the queries leaves the block in
+  // flight.
+  constexpr int NT = kVAW * AIO_WAVE;
+  constexpr int NQ = (kMaxRows * HD + NT - 1) / NT;
+  float qv[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int e = tid + i * NT, qq = e / HD, dim = e % HD;
+    qv[i] = e < M * HD ? a.q[(size_t)qq * a.H * HD + (size_t)h * HD + dim] : 0.f;
+  }
+  uint4 kr[NKC], vr[NVL];
+  int kb = kbA + wid;
+  vattn_load<HD>(kbase, vbase, max(min(kb, kbB - 1), 0), n_keys, lane, kr, vr);
+
+  // queries, scaled to log2 units and split into three bf16 terms
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int e = tid + i * NT, qq = e / HD, dim = e % HD;
+    if (e < M * HD) {
+      uint16_t t0, t1, t2;
+      split3(qv[i] * a.scale_log2, t0, t1, t2);
+      *(uint16_t*)(qs + (0 * Lds::QR + qq) * Lds::QROW + dim * 2) = t0;
+      *(uint16_t*)(qs + (1 * Lds::QR + qq) * Lds::QROW + dim * 2) = t1;
+      *(uint16_t*)(qs + (2 * Lds::QR + qq) * Lds::QROW + dim * 2) = t2;
+    }
+  }
+  for (int e = tid; e < 3 * HD; e += kVAW * AIO_WAVE)
+    *(uint16_t*)(qs + ((e / HD) * Lds::QR + kMaxRows) * Lds::QROW + (e % HD) * 2) = 0;
+  __syncthreads();
+
+  // this lane's query column rl: row rl sees keys [0, lim]
+  const bool live = rl < M;
+  const int lim = pos + (live ? rl : M - 1);
+  // lanes past the M rows read the zero row: their columns of S^T are zero
+  const char* qrow = qs + (live ? rl : kMaxRows) * Lds::QROW;
+  char* vt = tail + wid * Lds::VBYTES;
+  f32x16 o[NHB];
+#pragma unroll
+  for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[hb][i] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+
+  for (; kb < kbB; kb += kVAW) {
+    const int j0 = kb * 32;
+    // value rows -> LDS (a vector store: a uint4 struct copy is a memcpy,
+    // which keeps vr in scratch memory)
+#pragma unroll
+    for (int it = 0; it < NVL; ++it) {
+      const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
+      const u32x4 w = {vr[it].x, vr[it].y, vr[it].z, vr[it].w};
+      *(u32x4*)(vt + kk * Lds::VROW + d0 * 2) = w;
+    }
+    // scores S^T[key][query] over the HD dims, three query terms
+    f32x16 sc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+#pragma unroll
+    for (int c = 0; c < NKC; ++c) {
+      const bf16x8 ak = as_bf16x8(kr[c]);
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        const bf16x8 bq = as_bf16x8(
+            *(const uint4*)(qrow + t * Lds::QR * Lds::QROW + (c * 16 + 8 * kh) * 2));
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq, sc, 0, 0, 0);
+      }
+    }
+    // the next block's keys and values are in flight during the softmax and
+    // the P V product (the last block re-reads itself: no branch, so the
+    // fragments stay in registers)
+    vattn_load<HD>(kbase, vbase, kb + kVAW < kbB ? kb + kVAW : kb, n_keys, lane, kr, vr);
+    // causal mask (only a block holding keys past pos needs it; the test is
+    // the same for the whole wave) and online softmax for this lane's query
+    if (j0 + 31 > pos) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = j0 + 8 * (v / 4) + 4 * kh + (v % 4);
+        if (key > lim) sc[v] = -INFINITY;
+      }
+    }
+    float mx = sc[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sc[v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, AIO_WAVE));
+    const float mnew = fmaxf(m, mx);
+    // while every key so far is masked, mnew is -inf: subtract 0 instead, so
+    // exp2(-inf - 0) = 0 gives the zero weights (and o, lsum stay 0)
+    const float mref = mnew == -INFINITY ? 0.f : mnew;
+    const float cf = __builtin_amdgcn_exp2f(m - mref);
+    float p[16];
+    float ps = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      p[v] = __builtin_amdgcn_exp2f(sc[v] - mref);
+      ps += p[v];
+    }
+    lsum = lsum * cf + ps;
+    m = mnew;
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[hb][i] *= cf;
+    wave_lds_sync();  // the value tile is in LDS
+    // O^T += V^T P^T, two chunks of 16 keys, three terms of the weights.
+    // The weights split by truncation: t0 = the top 16 bits of p, t1 those
+    // of p - t0, t2 = p - t0 - t1 (exact: 8 significant bits each, 24 in
+    // all), without the rounding's branches.
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      uint32_t tt[3][8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t u0 = __float_as_uint(p[8 * c2 + e]) & 0xffff0000u;
+        const float r1 = p[8 * c2 + e] - __uint_as_float(u0);
+        const uint32_t u1 = __float_as_uint(r1) & 0xffff0000u;
+        const float r2 = r1 - __uint_as_float(u1);
+        tt[0][e] = u0;
+        tt[1][e] = u1;
+        tt[2][e] = __float_as_uint(r2);
+      }
+      bf16x8 bp[3];
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        bp[t] = as_bf16x8(make_uint4((tt[t][0] >> 16) | (tt[t][1] & 0xffff0000u),
+                                     (tt[t][2] >> 16) | (tt[t][3] & 0xffff0000u),
+                                     (tt[t][4] >> 16) | (tt[t][5] & 0xffff0000u),
+                                     (tt[t][6] >> 16) | (tt[t][7] & 0xffff0000u)));
+#pragma unroll
+      for (int hb = 0; hb < NHB; ++hb) {
+        // V^T fragment: dimension hb 32 + rl at this lane's eight keys
+        const char* vcol = vt + (hb * 32 + rl) * 2;
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          w[j] = (uint32_t)*(const uint16_t*)(vcol + vattn_key(c2, kh, 2 * j) * Lds::VROW) |
+                 ((uint32_t)*(const uint16_t*)(vcol + vattn_key(c2, kh, 2 * j + 1) * Lds::VROW)
+                  << 16);
+        const bf16x8 av = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+#pragma unroll
+        for (int t = 0; t < 3; ++t)
+          o[hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bp[t], o[hb], 0, 0, 0);
+      }
+    }
+    wave_lds_sync();  // every read of the value tile is done before the next block's writes
+  }
+  lsum += __shfl_xor(lsum, 32, AIO_WAVE);
+
+  // merge the waves' states: 2, 3 into 0, 1, then 1 into 0
+  __syncthreads();
+  float* om = (float*)tail;            // [2][32][OROW] outputs (rows padded: no bank conflicts)
+  float* mm = om + 2 * 32 * Lds::OROW;  // [2][32] max
+  float* ll = mm + 2 * 32;       // [2][32] sum
+  auto put = [&](int slot) {
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
+    if (kh == 0) {
+      mm[slot * 32 + rl] = m;
+      ll[slot * 32 + rl] = lsum;
+    }
+  };
+  auto take = [&](int slot) {
+    const float m2 = mm[slot * 32 + rl], l2 = ll[slot * 32 + rl];
+    const float Mx = fmaxf(m, m2);
+    const float c1 = m == -INFINITY ? 0.f : exp2f(m - Mx);
+    const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - Mx);
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        o[hb][v] = o[hb][v] * c1 +
+                   om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] * c2;
+    lsum = lsum * c1 + l2 * c2;
+    m = Mx;
+  };
+  if (wid >= 2) put(wid - 2);
+  __syncthreads();
+  if (wid < 2) take(wid);
+  __syncthreads();
+  if (wid == 1) put(0);
+  __syncthreads();
+  if (wid == 0) {
+    take(0);
+    put(1);  // slot 1 was taken by wave 1 before the last barrier
+  }
+  __syncthreads();
+
+  // The split's state of its M rows (unnormalized output, (max, sum) in
+  // log2 units), row by row from slot 1, written through to memory.
+  for (int e = tid; e < M * HD; e += NT) {
+    const int r = e / HD, dim = e % HD;
+    st_agent(a.part_o + (((size_t)r * a.H + h) * a.S + s) * HD + dim, om[(32 + r) * Lds::OROW + dim]);
+  }
+  if (tid < 2 * M) {
+    const int r = tid >> 1;
+    st_agent(a.part_ml + (((size_t)r * a.H + h) * a.S + s) * 2 + (tid & 1),
+             (tid & 1) ? ll[32 + r] : mm[32 + r]);
+  }
+  // count the split; the last of head h's splits to arrive merges them
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  __shared__ int last_s;
+  if (tid == 0) last_s = atomic_add_agent(a.cnt + h, 1) == a.S - 1;
+  __syncthreads();
+  if (!last_s) return;
+  if (tid == 0) atomic_store_agent(a.cnt + h, 0);  // ready for the next layer
+  vattn_merge<HD>(a, h, (float*)tail);
 }
 
 // Launch with `blocks` tile pairs.  A residual-add product with fewer tile
@@ -829,9 +989,19 @@ hipError_t launch_vnorm(const aio_model& m, float* x, const uint16_t* embed, con
   return hipGetLastError();
 }
 
+template <int HD>
+hipError_t launch_vattn_mma(const aio_model& m, const VAttnArgs& t) {
+  constexpr int lds = VAttnLds<HD>::BYTES;
+  const hipError_t e = hipFuncSetAttribute((const void*)k_vattn_mma<HD>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_vattn_mma<HD>, dim3(t.S, t.H), dim3(kVAW * AIO_WAVE), lds, m.stream, t);
+  return hipGetLastError();
+}
+
 }  // namespace
 
-hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
+hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits) {
   const aio_config& c = m.cfg;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int ka = m.lay.ka;
@@ -865,24 +1035,15 @@ hipError_t aio_launch_verify(const aio_model& m, int M, float* logits) {
     t.st = m.state();
     t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx; t.S = m.lay.splits; t.M = M;
     t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
-    // row groups of 3 up to 8K positions, of 5 beyond
-    const bool few = c.max_ctx <= 8192;
-    if (hd == 128 && few)
-      hipLaunchKernelGGL((k_vattn<128, 3, 2, false>), dim3(t.S, H), dim3(attn_block<3>()), 0,
-                         m.stream, t);
-    else if (hd == 128)
-      hipLaunchKernelGGL((k_vattn<128, 5, 4, true>), dim3(t.S, H), dim3(attn_block<5>()), 0,
-                         m.stream, t);
-    else if (few)
-      hipLaunchKernelGGL((k_vattn<64, 3, 2, false>), dim3(t.S, H), dim3(attn_block<3>()), 0,
-                         m.stream, t);
-    else
-      hipLaunchKernelGGL((k_vattn<64, 5, 4, true>), dim3(t.S, H), dim3(attn_block<5>()), 0,
-                         m.stream, t);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    VMergeArgs mg{t.part_o, t.part_ml, actB, ka, t.S, hd, H, M};
-    hipLaunchKernelGGL(k_vmerge, dim3(H, M), dim3(128), 0, m.stream, mg);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // splits of kVattnBlocksPerWave key blocks per wave (the host's pos
+    // sizes the grid; the kernel takes its key range from the device state)
+    const int nkb = (pos + M + 31) / 32;
+    t.S = std::max(1, std::min(m.lay.vsplits, (nkb + kVattnBlocksPerSplit - 1) / kVattnBlocksPerSplit));
+    t.cnt = m.at<int>(m.lay.vacnt);
+    t.act = actB;
+    t.lda = ka;
+    if ((e = hd == 128 ? launch_vattn_mma<128>(m, t) : launch_vattn_mma<64>(m, t)) != hipSuccess)
+      return e;
 
     VGemmArgs o{};
     o.act = actB; o.lda = ka; o.M = M;
