@@ -181,6 +181,11 @@ AIO_DEV int vk_hi(int block, int kh) { return WFMT == AIO_WFMT_BF16 ? block + 16
 // 16-byte skew per row, so that the fragment reads (32 rows at one column)
 // spread over the banks.  Stages of 1 KB per row (64 KB, one workgroup per
 // CU) measured slower: 5.16 against 4.89 ms per 7B bf16 verify.
+// Register sets of weight stages in flight per workgroup (three measured
+// slower: 4.56 against 4.20 ms per 7B bf16 verify, the extra registers
+// leaving one workgroup per CU).
+constexpr int kVNB = 2;
+
 template <int WFMT>
 struct VStage {
   static constexpr int KC = 256;                                     // k per stage
@@ -320,6 +325,16 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   const int ks = (int)blockIdx.y;
   const int kbA = ks * nkb / a.ks, kbB = (ks + 1) * nkb / a.ks;
   const int nst = (kbB - kbA + BPS - 1) / BPS;
+  // Workgroup b takes its stages starting at stage b mod nst (and wraps).
+  // Every row of W is K * wbytes apart, a multiple of the HBM channel
+  // interleave, so the same k offset of all rows lies in the same few
+  // channels: in step, every workgroup would read the same channels at
+  // once.
+  const int rot = nst > 0 ? (int)(blockIdx.x % (unsigned)nst) : 0;
+  auto kb0 = [&](int st) {  // first 32-k block of stage st (st < 2 nst)
+    const int p = st + rot;
+    return kbA + (p >= nst ? p - nst : p) * BPS;
+  };
   f32x16 acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t)
@@ -344,16 +359,18 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   // requested together, so waiting for one stage never waits for the
   // other stage's loads (vector loads complete in order); a block past the
   // slice re-reads the slice's last block and is not multiplied.
-  auto gload = [&](uint4 (&R)[St::NLD], uint4 (&A)[BPW][2], int st) {
+  auto gload_w = [&](uint4 (&R)[St::NLD], int st) {
 #pragma unroll
     for (int j = 0; j < St::NLD; ++j) {
-      int off = (kbA + st * BPS) * 32 * (int)wbytes + lchunk[j] * 16;
+      int off = kb0(st) * 32 * (int)wbytes + lchunk[j] * 16;
       off = off < kend ? off : kend;
       R[j] = ldg_nt(lrow[j] + off);
     }
+  };
+  auto gload_a = [&](uint4 (&A)[BPW][2], int st) {
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
-      const int block = min(kbA + st * BPS + wid + kGWaves * j, kbB - 1);
+      const int block = min(kb0(st) + wid + kGWaves * j, kbB - 1);
       A[j][0] = ldg(actp + vk_lo<WFMT>(block * 32, kh));
       A[j][1] = ldg(actp + vk_hi<WFMT>(block * 32, kh));
     }
@@ -361,7 +378,10 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   auto stage = [&](const uint4 (&R)[St::NLD]) {
     __syncthreads();  // every wave is done with the previous stage
 #pragma unroll
-    for (int j = 0; j < St::NLD; ++j) *(uint4*)(smem + lds_off[j]) = R[j];
+    for (int j = 0; j < St::NLD; ++j) {
+      const u32x4 w = {R[j].x, R[j].y, R[j].z, R[j].w};
+      *(u32x4*)(smem + lds_off[j]) = w;
+    }
     __syncthreads();
   };
   // Branch-free: a block past the slice multiplies zeros, so every path
@@ -371,7 +391,7 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
       const int wb = wid + kGWaves * j;
-      const bool live = col_live && kbA + st * BPS + wb < kbB;
+      const bool live = col_live && kb0(st) + wb < kbB;
       VFrag<WFMT, T> f;
 #pragma unroll
       for (int t = 0; t < T; ++t)
@@ -381,32 +401,46 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
       vmma(f, live, acc);
     }
   };
+  // One stage: its weights go to LDS, the register set is refilled with the
+  // weights kVNB stages ahead before the product (so kVNB stages stay in
+  // flight through it), and the activation fragments after it.  Loads past
+  // the slice re-read its last chunk.
+  auto step = [&](uint4 (&R)[St::NLD], uint4 (&A)[BPW][2], int st) {
+    stage(R);
+    __builtin_amdgcn_sched_barrier(0);
+    gload_w(R, st + kVNB);
+    __builtin_amdgcn_sched_barrier(0);
+    product(st, A);
+    __builtin_amdgcn_sched_barrier(0);
+    gload_a(A, st + kVNB);
+    __builtin_amdgcn_sched_barrier(0);
+  };
   if (nst > 0) {
-    // two stages in flight in registers: each set is refilled as soon as
-    // its stage has gone to LDS and been multiplied (the scheduling
-    // barriers keep that order)
-    uint4 R0[St::NLD], R1[St::NLD];
-    uint4 A0[BPW][2], A1[BPW][2];
-    gload(R0, A0, 0);
-    gload(R1, A1, 1);
+    uint4 R0[St::NLD], R1[St::NLD], R2[St::NLD];
+    uint4 A0[BPW][2], A1[BPW][2], A2[BPW][2];
+    gload_w(R0, 0);
+    gload_a(A0, 0);
+    gload_w(R1, 1);
+    gload_a(A1, 1);
+    if (kVNB > 2) {
+      gload_w(R2, 2);
+      gload_a(A2, 2);
+    }
     int st = 0;
-    for (; st + 2 < nst; st += 2) {
-      stage(R0);
-      product(st, A0);
-      __builtin_amdgcn_sched_barrier(0);
-      gload(R0, A0, st + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      stage(R1);
-      product(st + 1, A1);
-      __builtin_amdgcn_sched_barrier(0);
-      gload(R1, A1, st + 3);
-      __builtin_amdgcn_sched_barrier(0);
+    for (; st + kVNB < nst; st += kVNB) {
+      step(R0, A0, st);
+      step(R1, A1, st + 1);
+      if (kVNB > 2) step(R2, A2, st + 2);
     }
     stage(R0);
     product(st, A0);
     if (st + 1 < nst) {
       stage(R1);
       product(st + 1, A1);
+    }
+    if (kVNB > 2 && st + 2 < nst) {
+      stage(R2);
+      product(st + 2, A2);
     }
   }
   __syncthreads();  // the stage buffer becomes the partial-tile buffer
