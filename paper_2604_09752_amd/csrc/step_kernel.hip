@@ -916,9 +916,11 @@ AIO_DEV void attend_key(uint4 kk, uint4 vv, bool valid, const float (&q)[G][8],
     float sc = dot8_bf16(kk, make_float4(q[gg][0], q[gg][1], q[gg][2], q[gg][3]),
                          make_float4(q[gg][4], q[gg][5], q[gg][6], q[gg][7]), 0.f);
     sc = group_sum_dpp<LPK>(sc);
+    // exponents are <= 0 (the score or the old maximum minus the new one);
+    // the first valid key turns m = -inf into c = exp2(-inf) = 0
     const float mn = valid ? fmaxf(m[gg], sc) : m[gg];
-    const float c = valid ? exp2f(m[gg] - mn) : 1.f;
-    const float p = valid ? exp2f(sc - mn) : 0.f;
+    const float c = valid ? __builtin_amdgcn_exp2f(m[gg] - mn) : 1.f;
+    const float p = valid ? __builtin_amdgcn_exp2f(sc - mn) : 0.f;
     l[gg] = l[gg] * c + p;
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[gg][i] = fmaf(p, vf[i], o[gg][i] * c);
@@ -1141,10 +1143,15 @@ AIO_DEV void attn_phase(const MegaArgs& a, int layer, int pos, KV4& X, KV4& Y, f
       load4<HD>(u, Y, t + 12);
       __builtin_amdgcn_sched_barrier(0);
     }
+    // the last eight keys: slots past the wave's largest key count are
+    // skipped (a split of a few keys per group would otherwise spend most
+    // of its time on masked slots)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) attend_key<HD, G>(X.k[i], X.v[i], t + i < u.nk, q, o, m, l);
+    for (int i = 0; i < 4; ++i)
+      if (t + i < u.nkw) attend_key<HD, G>(X.k[i], X.v[i], t + i < u.nk, q, o, m, l);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < u.nk, q, o, m, l);
+    for (int i = 0; i < 4; ++i)
+      if (t + 4 + i < u.nkw) attend_key<HD, G>(Y.k[i], Y.v[i], t + 4 + i < u.nk, q, o, m, l);
     if (nw) {
       // the new key (position pos), taken by group 0 of the last split
       await16(a, nb, noff, nneed, nwd, vq);
