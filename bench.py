@@ -48,21 +48,18 @@ def workload_name(cfg) -> str:
                                         cfg.wfmt, cfg.prompt_len))
 
 
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_step_7b_2k_traffic.json")
-
-
 def measured_traffic(config: str, kernel_used: bool):
-    """HBM bytes per step-kernel launch from the committed counter record, or
-    None when the workload differs or the kernel's sources changed since."""
-    import hashlib
-    if config != "7b" or not kernel_used or not os.path.exists(TRAFFIC_RECORD):
+    """HBM bytes per step-kernel launch from the committed counter record of
+    this workload, or None when there is none or the kernel's sources changed
+    since it was taken."""
+    from paper_2604_09752_amd import profile_record
+    if not kernel_used or config not in profile_record.WORKLOADS:
         return None
-    rec = json.load(open(TRAFFIC_RECORD))
-    h = hashlib.sha256()
-    for f in rec["device_sources"]:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
-    if h.hexdigest() != rec["sources_sha256"]:
+    path = profile_record.record_path(config)
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("sources_sha256") != profile_record.sources_sha256():
         return None
     return int(rec["traffic_bytes_per_launch"])
 
