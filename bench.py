@@ -200,10 +200,20 @@ def probe_bench(n: int, reps: int = 5) -> int:
     ev1.record(dm.stream)
     dm.sync()
     ms = ev0.elapsed_time(ev1) / reps
-    cat_logits = lg[0].cpu().numpy()[labels]
+    # H(X) and the category on the device: only two floats cross to the host
+    hc = torch.zeros(2, dtype=torch.float32, device=dm.device)
+    binding.aio_category_entropy(dm.handle, lg[0], labels, hc)  # first launch loads the kernel
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    small, h, cat = binding.aio_probe_route(cat_logits, 0, n)
+    binding.aio_category_entropy(dm.handle, lg[0], labels, hc)
+    h_dev, cat_dev = [float(v) for v in hc.cpu().numpy()]
+    small = cat_dev == 0 and n <= 2048 and h_dev <= 0.45
     route_us = (time.perf_counter() - t0) * 1e6
+    # the host rule on the same logits gives the same values
+    _, h, cat = binding.aio_probe_route(lg[0].cpu().numpy()[labels], 0, n)
+    if abs(h - h_dev) > 1e-6 * max(1.0, abs(h)) or cat != int(cat_dev):
+        log("device entropy %r / category %r differ from the host's %r / %r" % (h_dev, cat_dev, h, cat))
+        return 3
     d, hd, L = cfg.d_model, cfg.head_dim, cfg.n_layers
     lin = L * (d * cfg.n_heads * hd + 2 * d * cfg.n_kv_heads * hd + cfg.n_heads * hd * d
                + 3 * d * cfg.ffn_dim)
@@ -213,8 +223,8 @@ def probe_bench(n: int, reps: int = 5) -> int:
            "tokens_per_s": round(n / ms * 1e3, 1),
            "algorithmic_tflops": round(flops / ms / 1e9, 1),
            "mfma_tflops": round((4 * n * lin + 2 * attn) / ms / 1e9, 1),
-           "entropy_nats": round(h, 4), "category": cat,
-           "route_to_small_model": small, "route_decision_us": round(route_us, 1),
+           "entropy_nats": round(h_dev, 4), "category": int(cat_dev),
+           "route_to_small_model": bool(small), "route_decision_us": round(route_us, 1),
            "workload": workload_name(cfg)}
     rc = 3 if dm.status() != 0 else 0
     dm.close()

@@ -366,6 +366,21 @@ int aio_probe_route(const float* category_logits, int32_t n_categories, int32_t 
                     int32_t ctx_len, int32_t ctx_limit, float tau, float* entropy,
                     int32_t* category);
 
+/* The probe's category scores on the device (Section 3.2): reads the
+ * logits of the n_labels label tokens label_ids[0 .. n_labels) (host array
+ * of vocabulary indices) from logits_dev (one fp32 row, e.g. what
+ * aio_prefill wrote) and writes out_dev[0] = H(X), the Shannon entropy in
+ * nats of their softmax, and out_dev[1] = the category (argmax, lowest index
+ * on ties) as a float; the same values aio_probe_route computes on the host
+ * from the same logits.  Enqueued on the model's stream; only the two floats
+ * need to cross to the host for the routing decision (Section 3.3).
+ * Returns AIO_EINVAL on null or misaligned pointers, AIO_ERANGE when
+ * n_labels is outside [1, AIO_MAX_CATEGORIES] or a label id outside
+ * [0, vocab). */
+#define AIO_MAX_CATEGORIES 64
+int aio_category_entropy(aio_model* m, const float* logits_dev, const int32_t* label_ids,
+                         int32_t n_labels, float* out_dev);
+
 /* ------------------------------------- draft-model speculative decoding */
 
 typedef struct aio_spec_stats {

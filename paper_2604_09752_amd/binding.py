@@ -99,6 +99,8 @@ def lib():
         L.aio_prefill.argtypes = [vp, vp, i32, i32, vp]
         L.aio_prefill_noalloc.argtypes = [vp, vp, i32, i32, vp]
         L.aio_prefill_noalloc_rows.argtypes = [P(aio_config)]
+        L.aio_category_entropy.argtypes = [vp, vp, vp, i32, vp]
+        L.aio_category_entropy.restype = i32
         L.aio_probe_route.argtypes = [vp, i32, i32, i32, i32, ctypes.c_float,
                                       P(ctypes.c_float), P(i32)]
         L.aio_spec_generate.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp,
@@ -294,6 +296,14 @@ def aio_probe_route(category_logits, code_category: int, ctx_len: int, ctx_limit
     if rc < 0:
         raise AioError(rc, "aio_probe_route")
     return bool(rc), float(h.value), int(cat.value)
+
+
+def aio_category_entropy(handle: int, logits: torch.Tensor, label_ids, out: torch.Tensor) -> None:
+    """Enqueue H(X) and the category of the label tokens' logits into out[0:2]
+    (device fp32)."""
+    ids = np.ascontiguousarray(label_ids, dtype=np.int32)
+    _check(lib().aio_category_entropy(handle, _ptr(logits), ids.ctypes.data, int(ids.size),
+                                      _ptr(out)), "aio_category_entropy")
 
 
 def aio_device_status(handle: int) -> int:

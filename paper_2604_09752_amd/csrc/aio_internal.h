@@ -115,6 +115,8 @@ hipError_t aio_launch_set_state(const aio_model& m, int32_t token, int32_t pos);
 hipError_t aio_launch_set_rows(const aio_model& m, const int32_t* toks, int rows, int32_t pos);
 hipError_t aio_launch_decode_layer(const aio_model& m, int l);
 hipError_t aio_launch_lm_head(const aio_model& m, float* logits);
+hipError_t aio_launch_category_entropy(const aio_model& m, const float* logits,
+                                       const int32_t* labels, int n, float* out);
 hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, int n,
                              int32_t* out, bool greedy_feedback);
 

@@ -732,6 +732,17 @@ int aio_probe_route(const float* category_logits, int32_t n_categories, int32_t 
   return best == code_category && ctx_len <= ctx_limit && h <= tau ? 1 : 0;
 }
 
+int aio_category_entropy(aio_model* m, const float* logits_dev, const int32_t* label_ids,
+                         int32_t n_labels, float* out_dev) {
+  if (!m || !logits_dev || !label_ids || !out_dev) return AIO_EINVAL;
+  if (((uintptr_t)logits_dev & 3u) || ((uintptr_t)out_dev & 3u)) return AIO_EINVAL;
+  if (n_labels < 1 || n_labels > AIO_MAX_CATEGORIES) return AIO_ERANGE;
+  for (int i = 0; i < n_labels; ++i)
+    if (label_ids[i] < 0 || label_ids[i] >= m->cfg.vocab) return AIO_ERANGE;
+  const hipError_t e = aio_launch_category_entropy(*m, logits_dev, label_ids, n_labels, out_dev);
+  return e == hipSuccess ? AIO_OK : hip_fail(e);
+}
+
 // ------------------------------------------------ draft-model speculation
 
 int aio_spec_generate(aio_model* target, aio_model* draft, int32_t pos, int32_t token,

@@ -433,6 +433,39 @@ __global__ __launch_bounds__(1024) void k_argmax(ArgmaxArgs a) {
   }
 }
 
+// The probe's category scores: the logits of up to kMaxCategories label
+// tokens.  One wave: lane i takes label i; the argmax (lowest index on ties)
+// and H = log Z - sum_i p_i (x_i - max), Z = sum_i e^(x_i - max), in double
+// and in label order (lane 0 folds the lanes' terms one by one), so the
+// value is the one the host routing rule computes from the same logits.
+constexpr int kMaxCategories = 64;
+struct CategoryArgs {
+  const float* logits;
+  int32_t label[kMaxCategories];
+  int n;
+  float* out;  // [0] = H in nats, [1] = category index (as a float)
+};
+
+__global__ __launch_bounds__(AIO_WAVE) void k_category_entropy(CategoryArgs a) {
+  __shared__ float xs[kMaxCategories];
+  const int i = threadIdx.x;
+  if (i < a.n) xs[i] = a.logits[a.label[i]];
+  __syncthreads();
+  if (i != 0) return;
+  int best = 0;
+  for (int j = 1; j < a.n; ++j)
+    if (xs[j] > xs[best]) best = j;
+  const double mx = xs[best];
+  double z = 0.0, ez = 0.0;
+  for (int j = 0; j < a.n; ++j) {
+    const double d = (double)xs[j] - mx, w = exp(d);
+    z += w;
+    ez += w * d;
+  }
+  a.out[0] = (float)(log(z) - ez / z);
+  a.out[1] = (float)best;
+}
+
 __global__ void k_set_state(aio_state* st, int32_t token, int32_t pos) {
   st->token[0] = token;
   st->pos = pos;
@@ -589,6 +622,18 @@ hipError_t aio_launch_lm_head(const aio_model& m, float* logits) {
   a.st = m.state();
   a.N = c.vocab; a.K = c.d_model; a.eps = c.rms_eps;
   return launch_gemv_fmt<EPI_STORE, AIO_R, AIO_U, true>(m, a, (c.vocab + AIO_R - 1) / AIO_R);
+}
+
+hipError_t aio_launch_category_entropy(const aio_model& m, const float* logits,
+                                       const int32_t* labels, int n, float* out) {
+  if (n < 1 || n > kMaxCategories) return hipErrorInvalidValue;
+  CategoryArgs a{};
+  a.logits = logits;
+  for (int i = 0; i < n; ++i) a.label[i] = labels[i];
+  a.n = n;
+  a.out = out;
+  hipLaunchKernelGGL(k_category_entropy, dim3(1), dim3(AIO_WAVE), 0, m.stream, a);
+  return hipGetLastError();
 }
 
 hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, int n,

@@ -117,6 +117,8 @@ def test_entry_points_reject_before_any_device_call(L):
     assert L.aio_decode_step(None, 0, 0, vp(16)) == B.AIO_EINVAL
     assert L.aio_verify(None, 0, None, 0, 0, vp(16)) == B.AIO_EINVAL
     assert L.aio_argmax(None, vp(16), 1, 1, vp(16)) == B.AIO_EINVAL
+    labels = (ctypes.c_int32 * 2)(0, 1)
+    assert L.aio_category_entropy(None, vp(16), labels, 2, vp(16)) == B.AIO_EINVAL
     assert L.aio_decode_greedy(None, 0, 0, 1, vp(16), vp(16)) == B.AIO_EINVAL
     out = (ctypes.c_int32 * 4)()
     assert L.aio_pld_generate(None, None, 0, 0, 4, 3, 1, 2, vp(16), vp(16), out,

@@ -102,3 +102,36 @@ def test_prefill_repeats_bit_for_bit():
         assert np.array_equal(outs[0][1], outs[1][1])
     finally:
         pair.close()
+
+
+def test_category_entropy_on_device_matches_host_rule():
+    """H(X) and the category of the label tokens' logits, computed on the
+    device (aio_category_entropy), equal the host routing rule's on the
+    same logits: prefill logits of a prompt, and planted cases (one
+    dominant label, two tied leaders, all equal)."""
+    import torch
+    from paper_2604_09752_amd import binding as B
+    cfg = TINY.with_(name="pf_entropy")
+    pair = Pair(cfg, with_oracle=False)
+    try:
+        toks = [int(t) for t in synth.make_prompt(cfg)[:40]]
+        pair.gpu.prefill(toks, 0, pair.logits)
+        pair.gpu.sync()
+        row = pair.logits[0]
+        out = torch.zeros(2, dtype=torch.float32, device=pair.gpu.device)
+        cases = [list(range(3)), [5, 17, 901, 2, 77], list(range(0, cfg.vocab, cfg.vocab // 40))]
+        planted = torch.zeros(cfg.vocab, dtype=torch.float32, device=pair.gpu.device)
+        planted[:8] = torch.tensor([3.0, 3.0, -1.0, 0.5, 0.5, 0.5, 0.5, 0.5])
+        for logits, labels in [(row, c) for c in cases] + [(planted, [0, 1, 2]), (planted, [3, 4, 5, 6])]:
+            B.aio_category_entropy(pair.gpu.handle, logits, labels, out)
+            pair.gpu.sync()
+            h_dev, cat_dev = [float(v) for v in out.cpu().numpy()]
+            _, h, cat = B.aio_probe_route(logits.cpu().numpy()[labels], 0, 10)
+            assert int(cat_dev) == cat
+            assert abs(h_dev - h) <= 1e-6 * max(1.0, abs(h)), (h_dev, h)
+        # all equal: ln C exactly as the host gives it
+        B.aio_category_entropy(pair.gpu.handle, planted, [3, 4, 5, 6], out)
+        pair.gpu.sync()
+        assert abs(float(out[0]) - np.log(4.0)) < 1e-6 and int(out[1]) == 0
+    finally:
+        pair.close()
