@@ -33,6 +33,10 @@ struct WsLayout {
   size_t vpart;    // fp32 [kVerifyMaxKs][MV][d] verify residual products split over K
   size_t vss;      // fp32 [MV][d/64]         verify rows' sums of squares per 64 columns
   size_t vcnt;     // int32 [d/64]            arrived K slices per column tile, zeroed at load
+  size_t pfix;     // fp32                    prefill K-slice partial tiles
+  size_t pfix_bytes;
+  size_t pcnt;     // int32 [pcnt_n]          arrived K slices per prefill tile, zeroed at load
+  size_t pcnt_n;
   size_t vacnt;    // int32 [H]               finished attention splits per head, zeroed at load
   size_t amax;     // int32 [MV]              argmax scratch
   size_t sync;     // uint32 [kSyncWords]     step-kernel barriers and counters

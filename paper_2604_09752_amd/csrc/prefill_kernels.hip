@@ -48,6 +48,22 @@ AIO_DEV void split3(float a, uint16_t& t0, uint16_t& t1, uint16_t& t2) {
 // The split of `a` into the term planes p[0], p[ts], p[2 ts].
 AIO_DEV void store_terms(uint16_t* p, size_t ts, float a) { split3(a, p[0], p[ts], p[2 * ts]); }
 
+// Device-coherent access for the K slices of a split product: the partials
+// are written through to memory and read past the (per-XCD) L2, and the
+// slice counters are vector atomics at device scope.
+AIO_DEV void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV float ld_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV int atomic_add_agent(int* p, int v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+AIO_DEV void atomic_store_agent(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Wait for this wave's LDS operations; also a compiler barrier, so no LDS
 // access moves across it.  Lanes of one wave exchange data through LDS
 // without a workgroup barrier (the waves of a workgroup run different
@@ -113,6 +129,7 @@ __global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
 // 16-byte skew), so the 32 rows a fragment read touches spread over the
 // banks.
 constexpr int kGT = 256;
+constexpr int kPfMaxKs = 8;  // most K slices of a prefill product
 constexpr int kBM = 128;  // weight rows per tile
 constexpr int kBR = 64;   // prompt rows per tile
 constexpr int kKT = 32;   // k per stage
@@ -146,6 +163,13 @@ struct PGemmArgs {
   uint16_t* vc;
   const float2* rope;   // [max_ctx][hd / 2] (cos, sin)
   int pos0, H, Hkv, hd, max_ctx;
+  // K split over workgroups (grid.z) when the tiles alone are too few: each
+  // slice writes its partial tile through to fix and counts itself in
+  // tcnt[tile]; the last slice to arrive adds the partials in slice order
+  // and runs the epilogue
+  int ks;
+  float* fix;           // [tiles][ks][kGT threads][32]
+  int* tcnt;            // [tiles], zero between products
 };
 
 // Where block `blk` (0..3) of tile `bx` reads its 32 rows: matrix index
@@ -309,22 +333,73 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[b][t][i] = 0.f;
 
-  const int nst = a.K / kKT;
-  gload_stage<WFMT, A_LD>(aptr, bptr, 0, ra_, rb_);
+  // this workgroup's stages [sA, sB) of K (all of them unless K is split)
+  const int nst = a.K / kKT, kz = (int)blockIdx.z;
+  const int sA = kz * nst / a.ks, sB = (kz + 1) * nst / a.ks;
+  gload_stage<WFMT, A_LD>(aptr, bptr, sA, ra_, rb_);
   lstore_stage<WFMT, A_LD>(smem, alds, blds, ra_, rb_);
   __syncthreads();
   // every stage but the last: the next stage's loads are in flight while the
   // current one is multiplied, then go to the other buffer
-  for (int st = 0; st + 1 < nst; ++st) {
+  for (int st = sA; st + 1 < sB; ++st) {
     gload_stage<WFMT, A_LD>(aptr, bptr, st + 1, ra_, rb_);
-    stage_product(smem + (st & 1) * kStageB, wn, wr, rl, kh, acc);
-    lstore_stage<WFMT, A_LD>(smem + ((st + 1) & 1) * kStageB, alds, blds, ra_, rb_);
+    stage_product(smem + ((st - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
+    lstore_stage<WFMT, A_LD>(smem + ((st + 1 - sA) & 1) * kStageB, alds, blds, ra_, rb_);
     __syncthreads();
   }
-  stage_product(smem + ((nst - 1) & 1) * kStageB, wn, wr, rl, kh, acc);
+  stage_product(smem + ((sB - 1 - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
 
-  // Epilogue.  D layout: lane l, register v -> column (prompt row) l % 32,
-  // row i = 8 (v / 4) + 4 (l / 32) + v % 4 of the 32-row block.
+  // the tile's sums over the three terms: lane l, register v -> column
+  // (prompt row) l % 32, row i = 8 (v / 4) + 4 (l / 32) + v % 4 of the
+  // 32-row blocks lo and hi
+  float ylo[16], yhi[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    ylo[v] = acc[0][0][v];
+    yhi[v] = acc[1][0][v];
+#pragma unroll
+    for (int t = 1; t < kNT; ++t) {
+      ylo[v] += acc[0][t][v];
+      yhi[v] += acc[1][t][v];
+    }
+  }
+  if (a.ks > 1) {
+    // K split: every slice's partial goes through memory (written through,
+    // read past the caches); the last slice to arrive adds them in slice
+    // order, so the sum is the same whatever the arrival order
+    const int tile = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+    float* mine = a.fix + (((size_t)tile * a.ks + kz) * kGT + tid) * 32;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      st_agent(mine + v, ylo[v]);
+      st_agent(mine + 16 + v, yhi[v]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    __shared__ int last_s;
+    if (tid == 0) last_s = atomic_add_agent(a.tcnt + tile, 1) == a.ks - 1;
+    __syncthreads();
+    if (!last_s) return;
+    if (tid == 0) atomic_store_agent(a.tcnt + tile, 0);  // ready for the next product
+#pragma unroll
+    for (int v = 0; v < 16; ++v) ylo[v] = yhi[v] = 0.f;
+    for (int k = 0; k < a.ks; ++k) {
+      const float* pk = a.fix + (((size_t)tile * a.ks + k) * kGT + tid) * 32;
+      float plo[16], phi[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        plo[v] = ld_agent(pk + v);
+        phi[v] = ld_agent(pk + 16 + v);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        ylo[v] += plo[v];
+        yhi[v] += phi[v];
+      }
+    }
+  }
+
+  // Epilogue.
   const int r = r0 + wr * 32 + rl;
   if (r >= a.R) return;
   const BlockSrc slo = block_src<EPI>(a, bx, 2 * wn);
@@ -332,12 +407,7 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int i = 8 * (v / 4) + 4 * kh + (v % 4);
-    float ylo = acc[0][0][v], yhi = acc[1][0][v];
-#pragma unroll
-    for (int t = 1; t < kNT; ++t) {
-      ylo += acc[0][t][v];
-      yhi += acc[1][t][v];
-    }
+    float ylo_v = ylo[v], yhi_v = yhi[v];
     if constexpr (EPI == PE_QKV) {
       if (slo.valid == 0) continue;
       const int half = a.hd / 2;
@@ -346,45 +416,45 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
       const int mat = slo.mat, row = slo.row0 + i;
       if constexpr (WFMT == AIO_WFMT_INT8) {
         const uint16_t* sc = mat == 0 ? a.s0 : (mat == 1 ? a.s1 : a.s2);
-        ylo *= fp16_to_f32(sc[row]);
-        yhi *= fp16_to_f32(sc[row + half]);
+        ylo_v *= fp16_to_f32(sc[row]);
+        yhi_v *= fp16_to_f32(sc[row + half]);
       }
       const int p = a.pos0 + r;
       if (mat < 2) {
         const float2 cs = a.rope[(size_t)p * half + ii];
-        const float r0v = ylo * cs.x - yhi * cs.y;
-        const float r1v = yhi * cs.x + ylo * cs.y;
-        ylo = r0v;
-        yhi = r1v;
+        const float r0v = ylo_v * cs.x - yhi_v * cs.y;
+        const float r1v = yhi_v * cs.x + ylo_v * cs.y;
+        ylo_v = r0v;
+        yhi_v = r1v;
       }
       if (mat == 0) {
-        a.out[(size_t)r * a.ldo + row] = ylo;
-        a.out[(size_t)r * a.ldo + row + half] = yhi;
+        a.out[(size_t)r * a.ldo + row] = ylo_v;
+        a.out[(size_t)r * a.ldo + row + half] = yhi_v;
       } else {
         const int g = row / a.hd;
         uint16_t* c = (mat == 1 ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
-        c[ii] = f32_to_bf16(ylo);
-        c[ii + half] = f32_to_bf16(yhi);
+        c[ii] = f32_to_bf16(ylo_v);
+        c[ii + half] = f32_to_bf16(yhi_v);
       }
     } else if constexpr (EPI == PE_SWIGLU) {
       if (i >= slo.valid) continue;
       const int n = slo.row0 + i;
       if constexpr (WFMT == AIO_WFMT_INT8) {
-        ylo *= fp16_to_f32(a.s0[n]);
-        yhi *= fp16_to_f32(a.s1[n]);
+        ylo_v *= fp16_to_f32(a.s0[n]);
+        yhi_v *= fp16_to_f32(a.s1[n]);
       }
       store_terms(a.act_out + (size_t)r * a.lda_out + n, a.tstride_out,
-                  ylo / (1.f + expf(-ylo)) * yhi);
+                  ylo_v / (1.f + expf(-ylo_v)) * yhi_v);
     } else {
       if (i < slo.valid) {
         const int n = slo.row0 + i;
-        if constexpr (WFMT == AIO_WFMT_INT8) ylo *= fp16_to_f32(a.s0[n]);
-        a.out[(size_t)r * a.ldo + n] += ylo;
+        if constexpr (WFMT == AIO_WFMT_INT8) ylo_v *= fp16_to_f32(a.s0[n]);
+        a.out[(size_t)r * a.ldo + n] += ylo_v;
       }
       if (i < shi.valid) {
         const int n = shi.row0 + i;
-        if constexpr (WFMT == AIO_WFMT_INT8) yhi *= fp16_to_f32(a.s0[n]);
-        a.out[(size_t)r * a.ldo + n] += yhi;
+        if constexpr (WFMT == AIO_WFMT_INT8) yhi_v *= fp16_to_f32(a.s0[n]);
+        a.out[(size_t)r * a.ldo + n] += yhi_v;
       }
     }
   }
@@ -410,29 +480,30 @@ template <int HD>
 struct AttnLds {
   static constexpr int QROW = HD * 2 + 16;        // bytes per query row of one term
   static constexpr int QBYTES = 3 * 32 * QROW;     // three terms of 32 queries
-  static constexpr int VROW = 32 * 2 + 16;         // bytes per hd row of a value tile
-  static constexpr int VBYTES = HD * VROW;         // one wave's transposed value tile
-  static constexpr int OBYTES = 2 * 32 * HD * 4 + 2 * 2 * 32 * 4;  // combine: 2 waves' O, m, l
+  static constexpr int VROW = HD * 2 + 16;         // bytes per key row of a value tile
+  static constexpr int VBYTES = 32 * VROW;         // one wave's value tile (32 keys)
+  static constexpr int OROW = HD + 1;              // floats per combined output row (padded)
+  static constexpr int OBYTES = 2 * 32 * OROW * 4 + 2 * 2 * 32 * 4;  // combine: 2 waves' O, m, l
   static constexpr int TAIL = kAW * VBYTES > OBYTES ? kAW * VBYTES : OBYTES;
   static constexpr int BYTES = QBYTES + TAIL;
 };
 
-// Position of key kk (0..31 of a block) in a transposed value row.  The
-// softmax weights reach the P V product as the B operand straight from the
-// score tile's registers: lane half kh of chunk c2 holds keys
-// 16 c2 + 4 kh + {0, 1, 2, 3, 8, 9, 10, 11}, so the value rows are stored in
-// that order and the A fragment is one 16-byte read.
-AIO_DEV int vpos(int kk) {
-  const int c2 = kk >> 4, w = kk & 15;
-  return c2 * 16 + ((w >> 2) & 1) * 8 + (w >> 3) * 4 + (w & 3);
-}
+// Key of element e (0..7) of lane half kh's softmax weights in 16-key chunk
+// c2.  The weights reach the P V product as the B operand straight from the
+// score tile's registers: score register v = 8 c2 + e holds key
+// 8 (v / 4) + 4 kh + v % 4, so the A fragment (V^T) gathers the value rows
+// of those keys.
+AIO_DEV int pkey(int c2, int kh, int e) { return 16 * c2 + 8 * (e >> 2) + 4 * kh + (e & 3); }
 
 // One workgroup per (32 query rows, head): wave w takes key blocks w, w + 4,
 // ... of 32 keys.  Per block: S^T = K Q^T on MFMA (A = 32 key rows from the
 // cache, B = the queries' three bf16 terms from LDS), the online softmax per
-// query (one query per lane pair), then O^T += V^T P^T (A = the transposed
-// value tile, B = the softmax weights' two terms from registers).  The
-// waves' (max, sum, output) states are merged through LDS at the end.
+// query (one query per lane pair), then O^T += V^T P^T (A = the value tile,
+// staged in LDS row by row and read back one bf16 per key and dimension; B =
+// the softmax weights' three terms from registers).  Transposing the value
+// tile on its way into LDS, one 16-bit store per element, put 16 lanes on
+// one bank.  The waves' (max, sum, output) states are merged through LDS at
+// the end.
 template <int HD>
 __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
   using Lds = AttnLds<HD>;
@@ -477,20 +548,16 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
 
   for (int kb = wid; kb < nkb; kb += kAW) {
     const int j0 = kb * 32;
-    // value rows -> LDS, transposed and permuted (16-byte chunks of 8 dims)
+    // value rows -> LDS, row by row (16-byte chunks of 8 dims; a vector
+    // store: a uint4 struct copy would go through scratch memory)
     constexpr int VCH = 32 * HD / 8;
 #pragma unroll
     for (int it = 0; it < VCH / AIO_WAVE; ++it) {
       const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
       const int key = j0 + kk < n_keys ? j0 + kk : 0;
       const uint4 w = *(const uint4*)(vbase + (size_t)key * HD + d0);
-      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-      char* col = vt + vpos(kk) * 2;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        *(uint16_t*)(col + (d0 + 2 * e) * Lds::VROW) = (uint16_t)(ww[e] & 0xffffu);
-        *(uint16_t*)(col + (d0 + 2 * e + 1) * Lds::VROW) = (uint16_t)(ww[e] >> 16);
-      }
+      const u32x4 wv = {w.x, w.y, w.z, w.w};
+      *(u32x4*)(vt + kk * Lds::VROW + d0 * 2) = wv;
     }
     // scores: S^T[key i][query j] over the HD dims, three query terms
     f32x16 s;
@@ -550,8 +617,14 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
                                      tt[t][6] | ((uint32_t)tt[t][7] << 16)));
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
-        const bf16x8 av =
-            as_bf16x8(*(const uint4*)(vt + (hb * 32 + rl) * Lds::VROW + (c2 * 16 + 8 * kh) * 2));
+        // V^T fragment: dimension hb 32 + rl at this lane's eight keys
+        const char* vcol = vt + (hb * 32 + rl) * 2;
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          w[j] = (uint32_t)*(const uint16_t*)(vcol + pkey(c2, kh, 2 * j) * Lds::VROW) |
+                 ((uint32_t)*(const uint16_t*)(vcol + pkey(c2, kh, 2 * j + 1) * Lds::VROW) << 16);
+        const bf16x8 av = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
 #pragma unroll
         for (int t = 0; t < 3; ++t) o[hb] = mfma(av, bp[t], o[hb]);
       }
@@ -562,15 +635,15 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
 
   // merge the waves' states: 2, 3 into 0, 1, then 1 into 0
   __syncthreads();
-  float* om = (float*)tail;                 // [2][32][HD] outputs
-  float* mm = om + 2 * 32 * HD;             // [2][32] max
+  float* om = (float*)tail;                 // [2][32][OROW] outputs (rows padded: no bank conflicts)
+  float* mm = om + 2 * 32 * Lds::OROW;      // [2][32] max
   float* ll = mm + 2 * 32;                  // [2][32] sum
   auto put = [&](int slot) {
 #pragma unroll
     for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
-        om[((size_t)slot * 32 + rl) * HD + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
+        om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
     if (kh == 0) {
       mm[slot * 32 + rl] = m;
       ll[slot * 32 + rl] = lsum;
@@ -586,7 +659,7 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v)
         o[hb][v] = o[hb][v] * c1 +
-                   om[((size_t)slot * 32 + rl) * HD + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] * c2;
+                   om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] * c2;
     lsum = lsum * c1 + l2 * c2;
     m = M;
   };
@@ -629,13 +702,28 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
   return hipGetLastError();
 }
 
+// Launch over `tiles` x (R / 64) tiles.  A residual product (O, down: d /
+// 128 tile columns) with fewer tiles than two per CU also splits K over
+// workgroups (up to kPfMaxKs slices of at least 8 stages), within the
+// fix-up buffer's room: 115 -> 85 us per product at 128 prompt rows.  The
+// QKV and gate/up products have 2-3x the tiles and lost more to the fix-up
+// (reading every slice's partial tile back) than they gained.
 template <int WFMT, int EPI>
-hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g, int tiles) {
+hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g0, int tiles) {
+  PGemmArgs g = g0;
+  const int rt = (g.R + kBR - 1) / kBR, nst = g.K / kKT;
+  g.ks = 1;
+  while (EPI == PE_RESID && tiles * rt * g.ks < 2 * m.num_cus && 2 * g.ks <= kPfMaxKs &&
+         nst / (2 * g.ks) >= 8 &&
+         (size_t)tiles * rt * 2 * g.ks * kGT * 32 * 4 <= m.lay.pfix_bytes &&
+         (size_t)tiles * rt <= m.lay.pcnt_n)
+    g.ks *= 2;
+  g.fix = m.at<float>(m.lay.pfix);
+  g.tcnt = m.at<int>(m.lay.pcnt);
   const void* fn = (const void*)k_pgemm<WFMT, EPI>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_pgemm<WFMT, EPI>), dim3(tiles, (g.R + kBR - 1) / kBR), dim3(kGT), kGemmLds,
-                     m.stream, g);
+  hipLaunchKernelGGL((k_pgemm<WFMT, EPI>), dim3(tiles, rt, g.ks), dim3(kGT), kGemmLds, m.stream, g);
   return hipGetLastError();
 }
 
