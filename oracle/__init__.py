@@ -76,6 +76,7 @@ def lib():
         L.orc_argmax.argtypes = [vp, ci]
         L.orc_argmax.restype = ci
         L.orc_decode_step.argtypes = [ctypes.POINTER(_Model), vp, ci, ci, vp]
+        L.orc_decode_step_row.argtypes = [ctypes.POINTER(_Model), vp, ci, ci, vp, vp, vp]
         L.orc_verify.argtypes = [ctypes.POINTER(_Model), vp, vp, ci, ci, vp]
         L.orc_num_threads.restype = ci
         _lib = L
@@ -207,6 +208,24 @@ class OracleModel:
         if rc:
             raise ValueError("oracle decode_step rejected token=%d pos=%d" % (token, pos))
         return logits
+
+    def decode_step_row(self, kv: np.ndarray, token: int, pos: int, row_in: np.ndarray):
+        """decode_step with the cache entries at ``pos`` taken from ``row_in``
+        (bf16 bits [n_layers][2][n_kv_heads][head_dim], any shape of that
+        size) in place of the step's own roundings, layer by layer before the
+        layer attends.  Returns (fp32 logits [V], the step's own row, same
+        layout as ``row_in``)."""
+        self._check_kv(kv)
+        c = self.cfg
+        rin = np.ascontiguousarray(row_in, dtype=np.uint16)
+        assert rin.size == c.n_layers * 2 * c.n_kv_heads * c.head_dim, rin.shape
+        own = np.empty_like(rin)
+        logits = np.empty(c.vocab, dtype=np.float32)
+        rc = lib().orc_decode_step_row(ctypes.byref(self._m), _p(kv), int(token), int(pos),
+                                       _p(rin), _p(own), _p(logits))
+        if rc:
+            raise ValueError("oracle decode_step rejected token=%d pos=%d" % (token, pos))
+        return logits, own
 
     def verify(self, kv: np.ndarray, toks, pos: int) -> np.ndarray:
         """Rows = toks at pos..pos+n-1; fp32 logits [n][V]."""

@@ -147,6 +147,11 @@ static const uint16_t* lin_scale(const orc_layer* L, int which) {
 }
 
 int orc_decode_step(const orc_model* m, uint16_t* kv, int token, int pos, float* logits) {
+  return orc_decode_step_row(m, kv, token, pos, NULL, NULL, logits);
+}
+
+int orc_decode_step_row(const orc_model* m, uint16_t* kv, int token, int pos,
+                        const uint16_t* row_in, uint16_t* row_out, float* logits) {
   const int d = m->d_model, H = m->n_heads, Hkv = m->n_kv_heads, hd = m->head_dim;
   const int F = m->ffn_dim, V = m->vocab, G = H / Hkv;
   if (token < 0 || token >= V || pos < 0 || pos >= m->max_ctx) return -1;
@@ -181,11 +186,18 @@ int orc_decode_step(const orc_model* m, uint16_t* kv, int token, int pos, float*
     /* 2c. RoPE on every query and key head at this position */
     for (int hh = 0; hh < H; ++hh) orc_rope(q + hh * hd, hd, pos, m->rope_base);
     for (int g = 0; g < Hkv; ++g) orc_rope(k + g * hd, hd, pos, m->rope_base);
-    /* 2d. append k, v to the bf16 cache at pos */
+    /* 2d. append k, v to the bf16 cache at pos (or the supplied row's entries,
+     * after handing out the step's own) */
+    const size_t row_l = (size_t)l * 2 * (size_t)(Hkv * hd);
     for (int g = 0; g < Hkv; ++g) {
       for (int i = 0; i < hd; ++i) {
-        Kc[(size_t)g * head_stride + (size_t)pos * hd + i] = orc_f32_to_bf16(k[g * hd + i]);
-        Vc[(size_t)g * head_stride + (size_t)pos * hd + i] = orc_f32_to_bf16(v[g * hd + i]);
+        uint16_t kb = orc_f32_to_bf16(k[g * hd + i]);
+        uint16_t vb = orc_f32_to_bf16(v[g * hd + i]);
+        const size_t rk = row_l + (size_t)(g * hd + i), rv = rk + (size_t)(Hkv * hd);
+        if (row_out) { row_out[rk] = kb; row_out[rv] = vb; }
+        if (row_in) { kb = row_in[rk]; vb = row_in[rv]; }
+        Kc[(size_t)g * head_stride + (size_t)pos * hd + i] = kb;
+        Vc[(size_t)g * head_stride + (size_t)pos * hd + i] = vb;
       }
     }
     /* 2e. each query head h attends over cached keys [0, pos] of kv head h/G */

@@ -77,6 +77,16 @@ int orc_argmax(const float* x, int n);
  * out-of-range token or position. */
 int orc_decode_step(const orc_model* m, uint16_t* kv, int token, int pos, float* logits);
 
+/* The same step with the entries cached at pos supplied from outside: the
+ * step's own bf16 K and V of every layer are written to row_out (layout
+ * [n_layers][2][n_kv_heads][head_dim]) and row_in's entries, not the step's,
+ * are stored at pos before that layer attends.  With row_in = the step's own
+ * row this is orc_decode_step exactly.  It lets a comparison start every
+ * position from identical state: a cache entry is a bf16 rounding, and two
+ * correct fp32 evaluations may round one entry to neighbouring values. */
+int orc_decode_step_row(const orc_model* m, uint16_t* kv, int token, int pos,
+                        const uint16_t* row_in, uint16_t* row_out, float* logits);
+
 /* rows = [tokens[0..n)] at positions pos..pos+n-1; logits fp32 [n][vocab]. */
 int orc_verify(const orc_model* m, uint16_t* kv, const int32_t* tokens, int n, int pos,
                float* logits);

@@ -5,14 +5,17 @@ Identical state.  Each compared step gives both sides the same token (the
 oracle's argmax of the step before: teacher forcing) and the same cache
 history: before the oracle computes position p, its cache rows for the
 positions this comparison already wrote are the GPU's rows, each of which
-was checked against the oracle's own row when it was written.  A cache row
-is the bf16 rounding of fp32 values that the two sides compute in different
-orders, so a value close to a rounding boundary may legitimately round to
-neighbouring bf16 values on the two sides; with int8 weights, whose
-attention is very peaked, one such flip of one entry moves the next logits
-by more than 2e-2 (pinned on the oracle alone in
-tests/test_int8_sensitivity.py).  So every step is compared from the same
-state, and the drift of free-running caches is logged beside it.
+was checked against the oracle's own row when it was written.  The row at p
+itself is the GPU's too: layer by layer the oracle rounds its own K and V
+(handed out for the check) and stores the GPU's entries before the layer
+attends.  A cache row is the bf16 rounding of fp32 values that the two sides
+compute in different orders, so a value close to a rounding boundary may
+legitimately round to neighbouring bf16 values on the two sides; with int8
+weights, whose attention is very peaked, one such flip of one entry moves
+the next logits by more than 2e-2 (pinned on the oracle alone in
+tests/test_int8_sensitivity.py), and a query that attends strongly to its
+own key moves its own logits the same way.  So every step is compared from
+the same state, and the drift of free-running caches is logged beside it.
 
 The bounds:
   * logits, bf16 weights: max-abs error <= 2e-2 over every logit of every
@@ -116,6 +119,11 @@ class Pair:
 
     def oracle_step(self, token: int, pos: int) -> np.ndarray:
         return self.orc.decode_step(self.kv_host, token, pos)
+
+    def oracle_step_row(self, token: int, pos: int, row: np.ndarray):
+        """The oracle's step with the GPU's cache row at pos in place of its
+        own roundings; returns (logits, the oracle's own row)."""
+        return self.orc.decode_step_row(self.kv_host, token, pos, row)
 
     def check_status(self):
         assert self.gpu.status() == 0, "a bounded wait of the step kernel gave up"
@@ -242,25 +250,27 @@ class Tally:
 def check_step(pair: Pair, g: np.ndarray, gi: int, tok: int, pos: int, what: str,
                tally: Tally, free_kv: np.ndarray | None = None) -> int:
     """Compares GPU logits g (and argmax gi) of consuming `tok` at `pos` with
-    the oracle's from identical state; then checks the cache row the GPU
-    wrote at pos against the oracle's and hands it to the oracle's cache.
+    the oracle's from identical state, the state including the cache row the
+    GPU wrote at pos (the oracle stores it in place of its own roundings,
+    layer by layer, before the layer attends); checks that row against the
+    oracle's own.
     With free_kv (a second oracle cache that is never forced) also logs the
     drift of free-running caches.  Returns the oracle's argmax."""
-    r = pair.oracle_step(tok, pos)
+    kg = pair.gpu.kv_rows(pos, pos + 1)
+    r, ko = pair.oracle_step_row(tok, pos, kg)
     ri = oracle.argmax(r)
     err, rms = compare_logits(g, r)
     gap = top2_gap(r)
     kind = check_argmax(gi, r, err, "%s pos %d" % (what, pos))
     tol = logit_tol(pair.cfg, rms)
     tally.kv_deep = kv_deep_abs(pair.cfg)
-    kg = pair.gpu.kv_rows(pos, pos + 1)
-    ko = pair.kv_host[:, :, :, pos:pos + 1, :]
+    ko = ko.reshape(kg.shape)
     need = kv_check(kg, ko, "%s pos %d" % (what, pos), tally.kv_deep)
     tally.kv_same += int((kg == ko).sum())
     tally.kv_total += kg.size
     tally.kv_need0 = max(tally.kv_need0, float(need[0]))
     tally.kv_need = max(tally.kv_need, float(need[1:].max()) if len(need) > 1 else 0.0)
-    pair.kv_host[:, :, :, pos:pos + 1, :] = kg
+    assert np.array_equal(pair.kv_host[:, :, :, pos:pos + 1, :], kg)
     free = ""
     if free_kv is not None:
         ef, _ = compare_logits(g, pair.orc.decode_step(free_kv, tok, pos))

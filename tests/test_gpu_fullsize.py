@@ -61,8 +61,13 @@ def test_fullsize_teacher_forced(name, n_steps):
         pair.close()
 
 
-def test_int8_verify_planted_3gram():
-    cfg = synth.CONFIGS["7b_int8"]
+@pytest.mark.parametrize("name", ["7b_int8", "7b", "1b"])
+def test_verify_planted_3gram(name):
+    """k = 8 verify of the planted 3-gram's drafts at the full shapes (the
+    launch configuration the verify bench times): every row's logits and
+    cache rows against the oracle from identical state, then the same
+    verify again, bit for bit."""
+    cfg = synth.CONFIGS[name]
     pair = Pair(cfg)
     try:
         P = cfg.prompt_len
@@ -70,8 +75,8 @@ def test_int8_verify_planted_3gram():
         _, drafts = synth.planted_drafts(cfg, synth.make_prompt(cfg), tau0)
         assert len(drafts) == 8
         tally = Tally()
-        got = check_verify(pair, tau0, drafts, P, "int8 verify", tally)
-        log("int8 verify: " + tally.summary())
+        got = check_verify(pair, tau0, drafts, P, name + " verify", tally)
+        log("%s verify: %s" % (name, tally.summary()))
         kv_rows = pair.gpu.kv_rows(P, P + 9)
         # the same verify again: bit-identical logits and cache rows
         pair.gpu.verify(tau0, drafts, P, pair.logits)

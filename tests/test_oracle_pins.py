@@ -312,6 +312,35 @@ def test_verify_equals_sequential_decode(oracle_lib):
     assert np.array_equal(kv1, kv2)
 
 
+def test_decode_step_row_supplied_entries(oracle_lib):
+    """The supplied-row step: given its own row back it is the plain step bit
+    for bit; given a row with one layer-0 V entry moved by one bf16 ulp, it
+    hands out the same layer-0 row, stores the supplied entries, and its
+    logits move (the attention reads the stored entry)."""
+    cfg = _small(prompt_len=12, n_steps=0, name="row")
+    m = oracle.OracleModel(cfg, synth.make_weights(cfg))
+    prompt = synth.make_prompt(cfg)
+    kv = synth.make_kv(cfg)
+    for p, t in enumerate(prompt[:-1]):
+        m.decode_step(kv, t, p)
+    pos, tok = len(prompt) - 1, prompt[-1]
+    kv_plain = kv.copy()
+    ref = m.decode_step(kv_plain, tok, pos)
+    own_plain = np.ascontiguousarray(kv_plain[:, :, :, pos, :])
+    kv_same = kv.copy()
+    lg, own = m.decode_step_row(kv_same, tok, pos, own_plain)
+    assert np.array_equal(lg.view(np.uint32), ref.view(np.uint32))
+    assert np.array_equal(own, own_plain)
+    assert np.array_equal(kv_same, kv_plain)
+    moved = own_plain.copy()
+    moved[0, 1, 0, 3] += 1
+    kv_moved = kv.copy()
+    lg2, own2 = m.decode_step_row(kv_moved, tok, pos, moved)
+    assert np.array_equal(own2[0], own_plain[0])
+    assert np.array_equal(kv_moved[:, :, :, pos, :], moved)
+    assert not np.array_equal(lg2, ref)
+
+
 def test_oracle_rejects_out_of_range(oracle_lib):
     cfg = _small(prompt_len=4, n_steps=0, name="r")
     m = oracle.OracleModel(cfg, synth.make_weights(cfg))
