@@ -33,6 +33,9 @@ struct WsLayout {
   size_t vpart;    // fp32 [kVerifyMaxKs][MV][d] verify residual products split over K
   size_t vss;      // fp32 [MV][d/64]         verify rows' sums of squares per 64 columns
   size_t vcnt;     // int32 [d/64]            arrived K slices per column tile, zeroed at load
+  size_t skpart;   // fp32 [sk_tiles][kVerifySkMaxC][AIO_MAX_VERIFY_ROWS*64] stream-K shared tile sums
+  size_t skcnt;    // int32 [sk_tiles]        arrived workgroups per shared tile pair, zeroed at load
+  size_t sk_tiles; // tile pairs of the largest stream-K product (QKV or gate/up)
   size_t pfix;     // fp32                    prefill K-slice partial tiles
   size_t pfix_bytes;
   size_t pcnt;     // int32 [pcnt_n]          arrived K slices per prefill tile, zeroed at load
@@ -59,6 +62,10 @@ struct WsLayout {
 // Largest number of K slices a verify residual product (O, down) is split
 // into; each slice's product goes to its own vpart slot.
 constexpr int kVerifyMaxKs = 8;
+
+// Most workgroups of a stream-K verify product (QKV, gate/up) that share
+// one tile pair; each has its slot of partial sums in skpart.
+constexpr int kVerifySkMaxC = 8;
 
 WsLayout aio_ws_layout(const aio_config& c);
 

@@ -102,6 +102,14 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.vpart = off; off = align256(off + (size_t)kVerifyMaxKs * MV * d * 4);
   L.vss = off; off = align256(off + MV * (d / 64) * 4);
   L.vcnt = off; off = align256(off + (d / 64) * 4);
+  {
+    const size_t qkv = ((size_t)c.n_heads + 2 * (size_t)c.n_kv_heads) * c.head_dim / 64;
+    const size_t gu = (F + 31) / 32;
+    L.sk_tiles = qkv > gu ? qkv : gu;
+  }
+  L.skpart = off;
+  off = align256(off + L.sk_tiles * kVerifySkMaxC * AIO_MAX_VERIFY_ROWS * 64 * 4);
+  L.skcnt = off; off = align256(off + L.sk_tiles * 4);
   // prefill K split (products with fewer tiles than two per CU): room for
   // 512 partial tiles of 128 x 64 fp32 and 1024 tile counters
   L.pfix_bytes = (size_t)512 * 128 * 64 * 4;
@@ -307,6 +315,7 @@ int aio_model_load(const aio_config* cfg, const aio_weights* w, void* kv_dev, vo
     }
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.sync, 0, (size_t)kSyncWords * 4);
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.vcnt, 0, (size_t)(cfg->d_model / 64) * 4);
+    if (e == hipSuccess) e = hipMemset(m->ws + m->lay.skcnt, 0, m->lay.sk_tiles * 4);
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.pcnt, 0, m->lay.pcnt_n * 4);
     if (e == hipSuccess) e = hipMemset(m->ws + m->lay.vacnt, 0, (size_t)cfg->n_heads * 4);
     if (e == hipSuccess)

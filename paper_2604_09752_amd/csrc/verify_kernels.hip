@@ -162,6 +162,12 @@ struct VGemmArgs {
   const uint16_t* g_next;
   uint16_t* act_next;
   float* ss_out;
+  // stream-K form (QKV, SWIGLU): tile pairs of the product, and the
+  // partial sums [tiles][kSkMaxC][kMaxRows * 64] and arrival counters
+  // [tiles] of tile pairs that several workgroups share
+  int tiles;
+  float* skpart;
+  int* skcnt;
 };
 
 // The k of the two MFMA fragments a lane holds in a block of 32 k (lane
@@ -257,6 +263,61 @@ template <int WFMT>
 constexpr int vgemm_lds() {
   return VStage<WFMT>::BYTES > kVRedBytes + kVFinBytes ? VStage<WFMT>::BYTES
                                                        : kVRedBytes + kVFinBytes;
+}
+
+// Epilogue of one output element of a QKV or gate/up tile pair tp (tile
+// row i, verify row r) from the pair's two norm-scaled sums y0, y1:
+//   QKV: rows (n, n + hd/2) of a head section, rotated at position pos + r,
+//     to q or to the K / V cache;
+//   SWIGLU: the same row n of gate and up, silu(g) u split into act_out.
+template <int WFMT, int EPI>
+AIO_DEV void vgemm_epi(const VGemmArgs& a, int tp, int r, int i, float y0, float y1, int pos) {
+  if constexpr (EPI == EPI_QKV) {
+    const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+    const int per_head = a.hd / 64;
+    const int head = tp / per_head, sub = tp % per_head;
+    const int ii = sub * 32 + i;  // index within the first half of the head
+    const int n_lo = head * a.hd + ii;
+    const int half = a.hd / 2;
+    float lo = y0, hi = y1;
+    if constexpr (WFMT == AIO_WFMT_INT8) {
+      // both rows of the pair lie in the same (q, k or v) section
+      const uint16_t* sc = a.s0;
+      int m_lo = n_lo;
+      if (n_lo >= qrows + krows) { sc = a.s2; m_lo -= qrows + krows; }
+      else if (n_lo >= qrows) { sc = a.s1; m_lo -= qrows; }
+      lo *= fp16_to_f32(sc[m_lo]);
+      hi *= fp16_to_f32(sc[m_lo + half]);
+    }
+    const int p = pos + r;
+    if (n_lo < qrows + krows) {
+      const float2 cs = a.rope[(size_t)p * half + ii];
+      const float r0 = lo * cs.x - hi * cs.y;
+      const float r1 = hi * cs.x + lo * cs.y;
+      lo = r0;
+      hi = r1;
+    }
+    if (n_lo < qrows) {
+      a.out[(size_t)r * a.ldo + n_lo] = lo;
+      a.out[(size_t)r * a.ldo + n_lo + half] = hi;
+    } else {
+      const bool is_k = n_lo < qrows + krows;
+      const int g = (n_lo - (is_k ? qrows : qrows + krows)) / a.hd;
+      uint16_t* c = (is_k ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
+      c[ii] = f32_to_bf16(lo);
+      c[ii + half] = f32_to_bf16(hi);
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    const int n = tp * 32 + i;
+    if (n < a.N) {
+      float g = y0, u = y1;
+      if constexpr (WFMT == AIO_WFMT_INT8) {
+        g *= fp16_to_f32(a.s0[n]);
+        u *= fp16_to_f32(a.s1[n]);
+      }
+      store_split(a.act_out, a.lda_out, a.M, r, n, g / (1.f + expf(-g)) * u);
+    }
+  }
 }
 
 template <int WFMT, int EPI>
@@ -492,51 +553,8 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
         s += red[w][t][i][r] + red[w][t][i][M + r] + red[w][t][i][2 * M + r];
       y[t] = EPI == EPI_RESID ? s : s * inv_s[r];
     }
-    if constexpr (EPI == EPI_QKV) {
-      const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
-      const int per_head = a.hd / 64;
-      const int head = blockIdx.x / per_head, sub = blockIdx.x % per_head;
-      const int ii = sub * 32 + i;  // index within the first half of the head
-      const int n_lo = head * a.hd + ii;
-      const int half = a.hd / 2;
-      float lo = y[0], hi = y[1];
-      if constexpr (WFMT == AIO_WFMT_INT8) {
-        // both rows of the pair lie in the same (q, k or v) section
-        const uint16_t* sc = a.s0;
-        int m_lo = n_lo;
-        if (n_lo >= qrows + krows) { sc = a.s2; m_lo -= qrows + krows; }
-        else if (n_lo >= qrows) { sc = a.s1; m_lo -= qrows; }
-        lo *= fp16_to_f32(sc[m_lo]);
-        hi *= fp16_to_f32(sc[m_lo + half]);
-      }
-      const int p = pos + r;
-      if (n_lo < qrows + krows) {
-        const float2 cs = a.rope[(size_t)p * half + ii];
-        const float r0 = lo * cs.x - hi * cs.y;
-        const float r1 = hi * cs.x + lo * cs.y;
-        lo = r0;
-        hi = r1;
-      }
-      if (n_lo < qrows) {
-        a.out[(size_t)r * a.ldo + n_lo] = lo;
-        a.out[(size_t)r * a.ldo + n_lo + half] = hi;
-      } else {
-        const bool is_k = n_lo < qrows + krows;
-        const int g = (n_lo - (is_k ? qrows : qrows + krows)) / a.hd;
-        uint16_t* c = (is_k ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
-        c[ii] = f32_to_bf16(lo);
-        c[ii + half] = f32_to_bf16(hi);
-      }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-      const int n = tile_row[0] + i;
-      if (n < a.N) {
-        float g = y[0], u = y[1];
-        if constexpr (WFMT == AIO_WFMT_INT8) {
-          g *= fp16_to_f32(a.s0[n]);
-          u *= fp16_to_f32(a.s1[n]);
-        }
-        store_split(a.act_out, a.lda_out, M, r, n, g / (1.f + expf(-g)) * u);
-      }
+    if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {
+      vgemm_epi<WFMT, EPI>(a, (int)blockIdx.x, r, i, y[0], y[1], pos);
     } else {
 #pragma unroll
       for (int t = 0; t < T; ++t) {
@@ -596,6 +614,296 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   }
 }
 
+// Stream-K form of the QKV and gate/up products.  The product's units, a
+// tile pair (64 weight rows) times a stage of 256 k, are dealt out in equal
+// contiguous ranges in (tile pair, stage) order, one range per workgroup and
+// one workgroup per CU: every CU streams the same number of bytes, and its
+// register pipeline (two stages in flight, as in k_vgemm) runs on across
+// tile-pair boundaries.  (With one whole tile pair per workgroup the gate /
+// up product has 344 workgroups for 256 CUs, and the CUs that hold two of
+// them set its length.)  A tile pair inside the range gets its epilogue as
+// soon as its last stage is multiplied; a pair the range shares with its
+// neighbours (at most one at each end) keeps its sums in registers until
+// the range is done, then writes them through to skpart at its slot (its
+// rank among the pair's workgroups) and counts itself in skcnt; the last to
+// arrive adds the slots in slot order, so the result does not depend on the
+// arrival order, and runs the epilogue.
+constexpr int kSkMaxC = kVerifySkMaxC;  // most workgroups sharing one tile pair
+
+template <int WFMT, int EPI>
+__global__ __launch_bounds__(kGBlock, 1) void k_vgemm_sk(VGemmArgs a) {
+  constexpr int T = 2;
+  using St = VStage<WFMT>;
+  extern __shared__ __align__(16) char smem[];
+  float (*red)[T][32][33] = (float (*)[T][32][33])smem;
+  __shared__ float inv_s[kMaxRows];
+  __shared__ int last_s[2];
+  const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
+  const int rl = lane & 31, kh = lane >> 5;
+  const size_t wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
+  const int M = a.M;
+  const bool col_live = rl < 3 * M;
+  constexpr int BPS = St::BPS, BPW = St::BPW;
+  const int nkb = a.K / 32;
+  const int nst = (nkb + BPS - 1) / BPS;
+  const long long U = (long long)a.tiles * nst, G = gridDim.x, gb = blockIdx.x;
+  const int u0 = (int)(gb * U / G), u1 = (int)((gb + 1) * U / G);
+  // workgroup whose range holds unit u
+  auto owner = [&](long long u) { return (int)(((u + 1) * G - 1) / U); };
+
+  // norm scales: requested first, reduced once the first stages are in flight
+  static_assert(kMaxRows <= 2 * kGWaves, "two rows per wave");
+  float ssp[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = wid + kGWaves * h;
+    if (r < M) {
+      const float* ssr = a.ss_in + (size_t)r * a.nt;
+      if (lane < a.nt) ssp[h][0] = ssr[lane];
+      if (lane + 64 < a.nt) ssp[h][1] = ssr[lane + 64];
+    }
+  }
+  const uint16_t* actp = a.act + (size_t)(col_live ? rl : 0) * a.lda;
+
+  // staging: load j of this thread is chunk lchunk[j] of stage row lrow[j]
+  // (row < 32: tile 0, else tile 1, of whichever pair the unit belongs to)
+  int lrow[St::NLD], lds_off[St::NLD], lchunk[St::NLD];
+#pragma unroll
+  for (int j = 0; j < St::NLD; ++j) {
+    const int f = j * kGBlock + tid;
+    lrow[j] = f / St::CPR;
+    lchunk[j] = f % St::CPR;
+    lds_off[j] = lrow[j] * St::RS + lchunk[j] * 16;
+  }
+  const int kend = nkb * 32 * (int)wbytes - 16;  // last 16-byte chunk of a row
+  const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
+  // first byte of weight row rr (0..63) of tile pair tp
+  auto row_ptr = [&](int tp, int rr) -> const char* {
+    const void* w;
+    int n;
+    if constexpr (EPI == EPI_QKV) {
+      const int per_head = a.hd / 64;
+      const int head = tp / per_head, sub = tp % per_head;
+      int n0 = head * a.hd + sub * 32;
+      w = a.w0;
+      if (n0 >= qrows + krows) { w = a.w2; n0 -= qrows + krows; }
+      else if (n0 >= qrows) { w = a.w1; n0 -= qrows; }
+      n = n0 + (rr >= 32 ? a.hd / 2 : 0) + (rr & 31);
+    } else {
+      w = rr >= 32 ? a.w1 : a.w0;
+      n = tp * 32 + (rr & 31);
+      if (n >= a.N) n = a.N - 1;
+    }
+    return (const char*)w + (size_t)n * a.K * wbytes;
+  };
+  // loads past the range re-read its last unit (and are not multiplied)
+  auto gload_w = [&](uint4 (&R)[St::NLD], int u) {
+    const int uu = u < u1 ? u : u1 - 1;
+    const int tp = uu / nst, s = uu - tp * nst;
+#pragma unroll
+    for (int j = 0; j < St::NLD; ++j) {
+      int off = s * St::KC * (int)wbytes + lchunk[j] * 16;
+      off = off < kend ? off : kend;
+      R[j] = ldg_nt(row_ptr(tp, lrow[j]) + off);
+    }
+  };
+  auto gload_a = [&](uint4 (&A)[BPW][2], int u) {
+    const int uu = u < u1 ? u : u1 - 1;
+    const int s = uu % nst;
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int block = min(s * BPS + wid + kGWaves * j, nkb - 1);
+      A[j][0] = ldg(actp + vk_lo<WFMT>(block * 32, kh));
+      A[j][1] = ldg(actp + vk_hi<WFMT>(block * 32, kh));
+    }
+  };
+  auto stage = [&](const uint4 (&R)[St::NLD]) {
+    __syncthreads();  // every wave is done with the previous stage
+#pragma unroll
+    for (int j = 0; j < St::NLD; ++j) {
+      const u32x4 w = {R[j].x, R[j].y, R[j].z, R[j].w};
+      *(u32x4*)(smem + lds_off[j]) = w;
+    }
+    __syncthreads();
+  };
+  f32x16 acc[T];
+  auto product = [&](int u, const uint4 (&A)[BPW][2]) {
+    const int s = u % nst;
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int wb = wid + kGWaves * j;
+      const bool live = col_live && s * BPS + wb < nkb;
+      VFrag<WFMT, T> f;
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+        frag_lds<WFMT>(smem + (t * 32 + rl) * St::RS, wb, kh, f.wa[t], f.wb[t]);
+      f.ba = __builtin_bit_cast(bf16x8, A[j][0]);
+      f.bb = __builtin_bit_cast(bf16x8, A[j][1]);
+      vmma(f, live, acc);
+    }
+  };
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
+  };
+  // The eight waves' sums of the current tile pair: element e = 32 r + i of
+  // this thread (e < 32 M), both tiles, three split terms added; raw (the
+  // norm scale comes later).
+  auto reduce = [&](float (&y)[T]) {
+    __syncthreads();  // the stage buffer becomes the partial-tile buffer
+    if (wid >= kGWaves / 2) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          red[wid - kGWaves / 2][t][8 * (v / 4) + 4 * kh + (v % 4)][rl] = acc[t][v];
+    }
+    __syncthreads();
+    if (wid < kGWaves / 2) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float& r = red[wid][t][8 * (v / 4) + 4 * kh + (v % 4)][rl];
+          r += acc[t][v];
+        }
+    }
+    __syncthreads();
+    const int i = tid % 32, r = tid / 32;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      float s = 0.f;
+      if (tid < 32 * M) {
+#pragma unroll
+        for (int w = 0; w < kGWaves / 2; ++w)
+          s += red[w][t][i][r] + red[w][t][i][M + r] + red[w][t][i][2 * M + r];
+      }
+      y[t] = s;
+    }
+    // the next stage() starts with a barrier: every read of red is done
+    // before the buffer is written again
+  };
+
+  uint4 R0[St::NLD], R1[St::NLD];
+  uint4 A0[BPW][2], A1[BPW][2];
+  gload_w(R0, u0);
+  gload_a(A0, u0);
+  gload_w(R1, u0 + 1);
+  gload_a(A1, u0 + 1);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = wid + kGWaves * h;
+    if (r < M) {
+      float p = ssp[h][0] + ssp[h][1];
+      for (int c = lane + 128; c < a.nt; c += 64) p += a.ss_in[(size_t)r * a.nt + c];
+      const float sum = wave_sum(p);
+      if (lane == 0) inv_s[r] = rsqrtf(sum / (float)a.K + a.eps);
+    }
+  }
+  const int pos = a.st->pos;
+  const int er = tid / 32, ei = tid % 32;  // this thread's epilogue element
+  // the range's shared tile pairs: [0] the one it starts in, [1] the one it
+  // ends in (-1: none)
+  int ptp[2] = {-1, -1};
+  float py[2][T] = {{0.f, 0.f}, {0.f, 0.f}};
+  zero_acc();
+  // After the product of unit u: if u ends a segment (the last unit of a
+  // tile pair or of the range), reduce it and finish or keep it.
+  auto seg_end = [&](int u) {
+    const int tp = u / nst;
+    if (u + 1 != u1 && u + 1 != (tp + 1) * nst) return;
+    float y[T];
+    reduce(y);
+    zero_acc();
+    const int sa = u0 > tp * nst ? u0 : tp * nst;  // first unit of the segment
+    const bool whole = sa == tp * nst && u + 1 == (tp + 1) * nst;
+    if (whole) {
+      if (tid < 32 * M)
+        vgemm_epi<WFMT, EPI>(a, tp, er, ei, y[0] * inv_s[er], y[1] * inv_s[er], pos);
+    } else if (sa == u0) {
+      ptp[0] = tp;
+      py[0][0] = y[0];
+      py[0][1] = y[1];
+    } else {
+      ptp[1] = tp;
+      py[1][0] = y[0];
+      py[1][1] = y[1];
+    }
+  };
+  auto step = [&](uint4 (&R)[St::NLD], uint4 (&A)[BPW][2], int u) {
+    stage(R);
+    __builtin_amdgcn_sched_barrier(0);
+    gload_w(R, u + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    product(u, A);
+    __builtin_amdgcn_sched_barrier(0);
+    gload_a(A, u + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    seg_end(u);
+  };
+  int u = u0;
+  for (; u + 2 <= u1; u += 2) {
+    step(R0, A0, u);
+    step(R1, A1, u + 1);
+  }
+  if (u < u1) {
+    stage(R0);
+    product(u, A0);
+    seg_end(u);
+  }
+
+  // shared tile pairs: write the sums through, count, and the last of the
+  // pair's workgroups adds the slots in order and finishes it
+  int slot[2], ncon[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    slot[p] = ncon[p] = 0;
+    if (ptp[p] < 0) continue;
+    const long long first = (long long)ptp[p] * nst;
+    const int g0 = owner(first), g1 = owner(first + nst - 1);
+    slot[p] = (int)gb - g0;
+    ncon[p] = g1 - g0 + 1;
+    if (tid < 32 * M) {
+      float* dst = a.skpart + ((size_t)ptp[p] * kSkMaxC + slot[p]) * (kMaxRows * 64) + er * 64 + ei;
+      st_agent(dst, py[p][0]);
+      st_agent(dst + 32, py[p][1]);
+    }
+  }
+  if (ptp[0] < 0 && ptp[1] < 0) return;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid < 2) {
+    last_s[tid] = 0;
+    if (ptp[tid] >= 0) last_s[tid] = atomic_add_agent(a.skcnt + ptp[tid], 1) == ncon[tid] - 1;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (!last_s[p]) continue;
+    if (tid == 0) atomic_store_agent(a.skcnt + ptp[p], 0);  // ready for the next product
+    if (tid < 32 * M) {
+      const float* src = a.skpart + (size_t)ptp[p] * kSkMaxC * (kMaxRows * 64) + er * 64 + ei;
+      float v0[kSkMaxC], v1[kSkMaxC];
+#pragma unroll
+      for (int k = 0; k < kSkMaxC; ++k) {
+        const int kk = k < ncon[p] ? k : 0;
+        v0[k] = ld_agent(src + (size_t)kk * (kMaxRows * 64));
+        v1[k] = ld_agent(src + (size_t)kk * (kMaxRows * 64) + 32);
+      }
+      float y0 = 0.f, y1 = 0.f;
+#pragma unroll
+      for (int k = 0; k < kSkMaxC; ++k)
+        if (k < ncon[p]) {
+          y0 += v0[k];
+          y1 += v1[k];
+        }
+      vgemm_epi<WFMT, EPI>(a, ptp[p], er, ei, y0 * inv_s[er], y1 * inv_s[er], pos);
+    }
+  }
+}
+
 // ------------------------------------------------------- causal attention
 
 struct VAttnArgs {
@@ -628,15 +936,17 @@ struct VAttnArgs {
 //     registers.  (Transposing on the way in, with one 16-bit store per
 //     element, put 16 lanes on one bank and tripled the kernel's time.)
 // The next block's keys and values are requested before the current one is
-// multiplied.  The waves' (max, sum, output) states merge through LDS; the
-// split's unnormalized state goes to part_o / part_ml, and the head's last
+// multiplied.  Every wave then leaves its (max, sum, output) state of the
+// live rows in LDS, and one pass combines the waves in wave order into the
+// split's unnormalized state, written to part_o / part_ml; the head's last
 // split to finish merges all of them (vattn_merge).
 //
-// Four blocks per wave and split measured best at 2K context: 3.20 ms per
-// int8 7B verify against 3.26 with two and 3.50 with one (more splits cost
-// more merging); at 32K the 64-split cap gives each wave 4 blocks as well.
-constexpr int kVAW = 4;
-constexpr int kVattnBlocksPerSplit = 4 * kVAW;
+// Eight waves of two blocks each: the blocks a wave streams one after the
+// other are the kernel's critical path (about 2 us each at 2K context), so
+// a split of 16 blocks is spread over as many waves as fit one workgroup
+// per CU with a block in flight per wave.
+constexpr int kVAW = 8;
+constexpr int kVattnBlocksPerSplit = 2 * kVAW;
 
 template <int HD>
 struct VAttnLds {
@@ -645,8 +955,8 @@ struct VAttnLds {
   static constexpr int QBYTES = 3 * QR * QROW;              // three terms of the M queries
   static constexpr int VROW = HD * 2 + 16;                  // bytes per key row of a value tile
   static constexpr int VBYTES = 32 * VROW;                  // one wave's value tile
-  static constexpr int OROW = HD + 1;                       // floats per merged output row
-  static constexpr int OBYTES = 2 * 32 * OROW * 4 + 2 * 2 * 32 * 4;  // merge: 2 waves' O, m, l
+  static constexpr int OROW = HD + 1;                       // floats per wave output row
+  static constexpr int OBYTES = kVAW * kMaxRows * OROW * 4 + 2 * kVAW * kMaxRows * 4;
   static constexpr int TAIL = kVAW * VBYTES > OBYTES ? kVAW * VBYTES : OBYTES;
   static constexpr int BYTES = QBYTES + TAIL;
 };
@@ -678,68 +988,54 @@ AIO_DEV void vattn_load(const uint16_t* kbase, const uint16_t* vbase, int kb, in
   }
 }
 
+// Online combination of one more (max m2, sum l2, output o2) state into
+// (m, l, o), all in log2 units; a state with max -inf holds no key.
+AIO_DEV void attn_fold(float& m, float& l, float& o, float m2, float l2, float o2) {
+  const float mn = fmaxf(m, m2);
+  const float c1 = m == -INFINITY ? 0.f : exp2f(m - mn);
+  const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - mn);
+  o = o * c1 + o2 * c2;
+  l = l * c1 + l2 * c2;
+  m = mn;
+}
+
 // Merge of head h's S splits for the M rows (by the split that finished
-// last; the others' states are in memory, read past the caches):
-// o_r = sum_s w_rs o_rs with w_rs = 2^(m_rs - max_s m_rs) / L_r and
-// L_r = sum_s 2^(m_rs - max) l_rs, in split order; o_r is split into act.
-// `ws` is LDS for 3 M S + ... floats (the weights, padded to 8 splits).
+// last; the others' states are in memory, read past the caches): per output
+// element, the splits' states are folded in split order (attn_fold) and the
+// result o / l is split into act.  Eight splits' states are requested
+// together, so at up to 8 splits the merge is one round trip.
 template <int HD>
-AIO_DEV void vattn_merge(const VAttnArgs& a, int h, float* ws) {
+AIO_DEV void vattn_merge(const VAttnArgs& a, int h) {
   constexpr int NT = kVAW * AIO_WAVE;
-  const int tid = threadIdx.x, M = a.M, S = a.S;
-  const int S8 = (S + 7) & ~7;
-  float* mS = ws;            // [M][S8]
-  float* lS = mS + M * S8;   // [M][S8]
-  float* w = lS + M * S8;    // [M][S8] merge weights, 0 past S
-  for (int t = tid; t < M * S8; t += NT) {
-    const int r = t / S8, sp = t % S8;
-    float mv = -INFINITY, lv = 0.f;
-    if (sp < S) {
-      const float* ml = a.part_ml + (((size_t)r * a.H + h) * S + sp) * 2;
-      mv = ld_agent(ml);
-      lv = ld_agent(ml + 1);
-    }
-    mS[t] = mv;
-    lS[t] = lv;
-  }
-  __syncthreads();
-  if (tid < M) {
-    float mx = -INFINITY;
-    for (int sp = 0; sp < S; ++sp) mx = fmaxf(mx, mS[tid * S8 + sp]);
-    float L = 0.f;
-    for (int sp = 0; sp < S; ++sp) {
-      const float ms = mS[tid * S8 + sp];
-      if (ms != -INFINITY) L = fmaf(exp2f(ms - mx), lS[tid * S8 + sp], L);
-    }
-    for (int sp = 0; sp < S8; ++sp) {
-      const float ms = mS[tid * S8 + sp];
-      w[tid * S8 + sp] = ms == -INFINITY ? 0.f : exp2f(ms - mx) / L;
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < M * HD; e += NT) {
+  const int M = a.M, S = a.S;
+  for (int e = threadIdx.x; e < M * HD; e += NT) {
     const int r = e / HD, dim = e % HD;
     const float* po = a.part_o + ((size_t)r * a.H + h) * S * HD + dim;
-    const float* wr = w + r * S8;
-    float o = 0.f;
-    for (int s0 = 0; s0 < S8; s0 += 8) {
-      // eight splits' values requested together (past S: split 0, weight 0)
-      float v[8];
+    const float* ml = a.part_ml + ((size_t)r * a.H + h) * S * 2;
+    float m = -INFINITY, l = 0.f, o = 0.f;
+    for (int s0 = 0; s0 < S; s0 += 8) {
+      float mv[8], lv[8], ov[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ld_agent(po + (size_t)(s0 + j < S ? s0 + j : 0) * HD);
+      for (int j = 0; j < 8; ++j) {
+        const int sp = s0 + j < S ? s0 + j : S - 1;
+        mv[j] = ld_agent(ml + 2 * sp);
+        lv[j] = ld_agent(ml + 2 * sp + 1);
+        ov[j] = ld_agent(po + (size_t)sp * HD);
+      }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) o = fmaf(wr[s0 + j], v[j], o);
+      for (int j = 0; j < 8; ++j)
+        if (s0 + j < S) attn_fold(m, l, o, mv[j], lv[j], ov[j]);
     }
-    store_split(a.act, a.lda, M, r, h * HD + dim, o);
+    store_split(a.act, a.lda, M, r, h * HD + dim, l > 0.f ? o / l : 0.f);
   }
 }
 
 template <int HD>
-__global__ __launch_bounds__(kVAW * AIO_WAVE, 2) void k_vattn_mma(VAttnArgs a) {
+__global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
   using Lds = VAttnLds<HD>;
   extern __shared__ __align__(16) char smem[];
   char* qs = smem;                  // [3][QR][QROW]; row kMaxRows of each term is zero
-  char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the merge
+  char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the waves' states
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
   const int rl = lane & 31, kh = lane >> 5;
   const int s = blockIdx.x, h = blockIdx.y, M = a.M;
@@ -781,7 +1077,7 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 2) void k_vattn_mma(VAttnArgs a) {
       *(uint16_t*)(qs + (2 * Lds::QR + qq) * Lds::QROW + dim * 2) = t2;
     }
   }
-  for (int e = tid; e < 3 * HD; e += kVAW * AIO_WAVE)
+  for (int e = tid; e < 3 * HD; e += NT)
     *(uint16_t*)(qs + ((e / HD) * Lds::QR + kMaxRows) * Lds::QROW + (e % HD) * 2) = 0;
   __syncthreads();
 
@@ -902,58 +1198,40 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 2) void k_vattn_mma(VAttnArgs a) {
   }
   lsum += __shfl_xor(lsum, 32, AIO_WAVE);
 
-  // merge the waves' states: 2, 3 into 0, 1, then 1 into 0
+  // every wave's state of the live rows -> LDS (over the value tiles)
   __syncthreads();
-  float* om = (float*)tail;            // [2][32][OROW] outputs (rows padded: no bank conflicts)
-  float* mm = om + 2 * 32 * Lds::OROW;  // [2][32] max
-  float* ll = mm + 2 * 32;       // [2][32] sum
-  auto put = [&](int slot) {
+  float* om = (float*)tail;                    // [kVAW][kMaxRows][OROW] outputs
+  float* mm = om + kVAW * kMaxRows * Lds::OROW;  // [kVAW][kMaxRows] max
+  float* ll = mm + kVAW * kMaxRows;            // [kVAW][kMaxRows] sum
+  if (live) {
 #pragma unroll
     for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
-        om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
+        om[(wid * kMaxRows + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
     if (kh == 0) {
-      mm[slot * 32 + rl] = m;
-      ll[slot * 32 + rl] = lsum;
+      mm[wid * kMaxRows + rl] = m;
+      ll[wid * kMaxRows + rl] = lsum;
     }
-  };
-  auto take = [&](int slot) {
-    const float m2 = mm[slot * 32 + rl], l2 = ll[slot * 32 + rl];
-    const float Mx = fmaxf(m, m2);
-    const float c1 = m == -INFINITY ? 0.f : exp2f(m - Mx);
-    const float c2 = m2 == -INFINITY ? 0.f : exp2f(m2 - Mx);
-#pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        o[hb][v] = o[hb][v] * c1 +
-                   om[((size_t)slot * 32 + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] * c2;
-    lsum = lsum * c1 + l2 * c2;
-    m = Mx;
-  };
-  if (wid >= 2) put(wid - 2);
-  __syncthreads();
-  if (wid < 2) take(wid);
-  __syncthreads();
-  if (wid == 1) put(0);
-  __syncthreads();
-  if (wid == 0) {
-    take(0);
-    put(1);  // slot 1 was taken by wave 1 before the last barrier
   }
   __syncthreads();
 
-  // The split's state of its M rows (unnormalized output, (max, sum) in
-  // log2 units), row by row from slot 1, written through to memory.
+  // The split's state of its M rows: the waves folded in wave order
+  // (unnormalized output, (max, sum) in log2 units), written through to
+  // memory.
   for (int e = tid; e < M * HD; e += NT) {
     const int r = e / HD, dim = e % HD;
-    st_agent(a.part_o + (((size_t)r * a.H + h) * a.S + s) * HD + dim, om[(32 + r) * Lds::OROW + dim]);
-  }
-  if (tid < 2 * M) {
-    const int r = tid >> 1;
-    st_agent(a.part_ml + (((size_t)r * a.H + h) * a.S + s) * 2 + (tid & 1),
-             (tid & 1) ? ll[32 + r] : mm[32 + r]);
+    float ms = -INFINITY, ls = 0.f, os = 0.f;
+#pragma unroll
+    for (int w = 0; w < kVAW; ++w)
+      attn_fold(ms, ls, os, mm[w * kMaxRows + r], ll[w * kMaxRows + r],
+                om[(w * kMaxRows + r) * Lds::OROW + dim]);
+    st_agent(a.part_o + (((size_t)r * a.H + h) * a.S + s) * HD + dim, os);
+    if (dim == 0) {
+      float* ml = a.part_ml + (((size_t)r * a.H + h) * a.S + s) * 2;
+      st_agent(ml, ms);
+      st_agent(ml + 1, ls);
+    }
   }
   // count the split; the last of head h's splits to arrive merges them
   __builtin_amdgcn_s_waitcnt(0);
@@ -963,7 +1241,7 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 2) void k_vattn_mma(VAttnArgs a) {
   __syncthreads();
   if (!last_s) return;
   if (tid == 0) atomic_store_agent(a.cnt + h, 0);  // ready for the next layer
-  vattn_merge<HD>(a, h, (float*)tail);
+  vattn_merge<HD>(a, h);
 }
 
 // Launch with `blocks` tile pairs.  A residual-add product with fewer tile
@@ -1001,6 +1279,43 @@ hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
                                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_vgemm<AIO_WFMT_BF16, EPI>), grid, dim3(kGBlock), lds, m.stream, a);
+  }
+  return hipGetLastError();
+}
+
+// Stream-K launch of a QKV or gate/up product of `tiles` tile pairs: one
+// workgroup per CU, but every range at least `per` units long, so that at
+// most kSkMaxC - 1 ranges meet in one tile pair (a pair of nst units spans
+// at most 1 + ceil((nst - 1) / per) ranges).
+template <int EPI>
+hipError_t launch_vgemm_sk(const aio_model& m, const VGemmArgs& g, int tiles) {
+  VGemmArgs a = g;
+  a.ks = 1;
+  a.nt = m.cfg.d_model / 64;
+  a.eps = m.cfg.rms_eps;
+  a.ss_in = m.at<float>(m.lay.vss);
+  a.tiles = tiles;
+  a.skpart = m.at<float>(m.lay.skpart);
+  a.skcnt = m.at<int>(m.lay.skcnt);
+  if ((size_t)tiles > m.lay.sk_tiles) return hipErrorInvalidValue;
+  const int nst = (a.K / 32 + 7) / 8;  // stages of 256 k
+  const long long U = (long long)tiles * nst;
+  const int per = std::max(2, (nst - 1 + kSkMaxC - 3) / (kSkMaxC - 2));
+  const long long G = std::max<long long>(1, std::min<long long>(m.num_cus, U / per));
+  if (m.cfg.wfmt == AIO_WFMT_INT8) {
+    constexpr int lds = vgemm_lds<AIO_WFMT_INT8>();
+    const hipError_t e = hipFuncSetAttribute((const void*)k_vgemm_sk<AIO_WFMT_INT8, EPI>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_vgemm_sk<AIO_WFMT_INT8, EPI>), dim3((unsigned)G), dim3(kGBlock), lds,
+                       m.stream, a);
+  } else {
+    constexpr int lds = vgemm_lds<AIO_WFMT_BF16>();
+    const hipError_t e = hipFuncSetAttribute((const void*)k_vgemm_sk<AIO_WFMT_BF16, EPI>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_vgemm_sk<AIO_WFMT_BF16, EPI>), dim3((unsigned)G), dim3(kGBlock), lds,
+                       m.stream, a);
   }
   return hipGetLastError();
 }
@@ -1091,7 +1406,7 @@ hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits) 
     gu.w0 = L.w_gate; gu.w1 = L.w_up;
     gu.s0 = (const uint16_t*)L.s_gate; gu.s1 = (const uint16_t*)L.s_up;
     gu.N = F; gu.K = d; gu.act_out = actB; gu.lda_out = ka; gu.st = m.state();
-    if ((e = launch_vgemm<EPI_SWIGLU>(m, gu, (F + 31) / 32)) != hipSuccess) return e;
+    if ((e = launch_vgemm_sk<EPI_SWIGLU>(m, gu, (F + 31) / 32)) != hipSuccess) return e;
 
     VGemmArgs dn{};
     dn.act = actB; dn.lda = ka; dn.M = M;

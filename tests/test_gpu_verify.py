@@ -25,6 +25,11 @@ CASES = {
     # O (K = 1024) and down (K = 4096) products split over K, their slices
     # added in order by the next RMSNorm
     "split_k": dict(n_heads=16, n_kv_heads=4, ffn_dim=4096),
+    # d 576: three 256-k stages per tile pair, the last one ragged; the QKV
+    # and gate/up products deal out (tile pair, stage) units two per
+    # workgroup, so tile pairs are shared by two workgroups
+    "stream_k": dict(d_model=576, ffn_dim=192),
+    "stream_k_int8": dict(d_model=576, ffn_dim=192, wfmt="int8"),
 }
 
 
