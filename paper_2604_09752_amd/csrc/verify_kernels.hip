@@ -924,17 +924,24 @@ struct VAttnArgs {
 
 // Causal attention of the M verify rows on MFMA.  One workgroup of kVAW
 // waves per (split s, query head h); the split takes key blocks [kbA, kbB)
-// of 32 keys, and wave w the blocks kbA + w, kbA + w + kVAW, ...  Per block:
-//   S^T = K Q^T: A = 32 key rows straight from the cache (exact bf16), B =
-//     the M queries' three bf16 terms (log2-scaled) from LDS; lanes past M
-//     multiply zeros.  The three terms accumulate into one tile, so column r
-//     of S^T is row r's scores in fp32-level precision.
-//   online softmax per query column (causal mask j <= pos + r);
-//   O^T += V^T P^T: A = the value tile (staged in LDS row by row, read back
-//     one bf16 per key and dimension, in the order the score registers hold
-//     the keys), B = the softmax weights' three bf16 terms straight from
-//     registers.  (Transposing on the way in, with one 16-bit store per
-//     element, put 16 lanes on one bank and tripled the kernel's time.)
+// of 32 keys, and wave w the blocks kbA + w, kbA + w + kVAW, ...  The
+// products are 16 x 16 x 32 MFMAs (lane l: row or column l % 16 of a tile,
+// k = 8 (l / 16) .. + 7 of the operands, rows 4 (l / 16) .. + 3 of the
+// result): 16 query columns cover the M <= 10 rows with half the dead work
+// of a 32-column tile.  Per block:
+//   S^T = K Q^T, two tiles of 16 keys: A = key rows straight from the cache
+//     (exact bf16), B = the M queries' three bf16 terms (log2-scaled) from
+//     LDS; columns past M multiply zeros.  The three terms accumulate into
+//     one tile, so column r of S^T is row r's scores in fp32-level
+//     precision.  Lane l holds keys 4 (l / 16) .. + 3 of both tiles;
+//   online softmax per query column (causal mask j <= pos + r), the max
+//     over a column's four lane groups by two exchanges;
+//   O^T += V^T P^T: B = the softmax weights' three bf16 terms straight from
+//     registers (k slots 8 g .. 8 g + 7 of lane group g are its own keys of
+//     tile 0 then tile 1), A = the value tile (staged in LDS row by row,
+//     read back one bf16 per key and dimension in that key order).
+//     (Transposing on the way in, with one 16-bit store per element, put
+//     16 lanes on one bank and tripled the kernel's time.)
 // The next block's keys and values are requested before the current one is
 // multiplied.  Every wave then leaves its (max, sum, output) state of the
 // live rows in LDS, and one pass combines the waves in wave order into the
@@ -961,25 +968,31 @@ struct VAttnLds {
   static constexpr int BYTES = QBYTES + TAIL;
 };
 
-// Key of element e (0..7) of lane half kh's softmax weights in 16-key chunk
-// c2: score register v = 8 c2 + e holds key 8 (v / 4) + 4 kh + v % 4.
-AIO_DEV int vattn_key(int c2, int kh, int e) { return 16 * c2 + 8 * (e >> 2) + 4 * kh + (e & 3); }
+// Key (within the block) of k slot 8 g + j of the P V product: the softmax
+// weight register j of lane group g, keys 4 g .. + 3 of tile 0, then of tile 1.
+AIO_DEV int vattn_key(int g, int j) { return 16 * (j >> 2) + 4 * g + (j & 3); }
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 AIO_DEV bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
 // Wait for this wave's LDS operations (also a compiler barrier for LDS).
 AIO_DEV void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// Block kb's key fragments (A operand: key row rl, dims 16 c + 8 kh ..) and
-// value chunks (16 bytes each, row-major); keys past n_keys read key 0.
+// Block kb's key fragments (A operand of tile tt: key row 16 tt + l % 16,
+// dims 32 c + 8 (l / 16) ..) and value chunks (16 bytes each, row-major);
+// keys past n_keys read key 0.
 template <int HD>
 AIO_DEV void vattn_load(const uint16_t* kbase, const uint16_t* vbase, int kb, int n_keys,
                         int lane, uint4 (&kr)[HD / 16], uint4 (&vr)[32 * HD / 8 / AIO_WAVE]) {
-  const int rl = lane & 31, kh = lane >> 5, j0 = kb * 32;
-  const int key = j0 + rl < n_keys ? j0 + rl : 0;
-  const uint16_t* krow = kbase + (size_t)key * HD;
+  const int r16 = lane & 15, g = lane >> 4, j0 = kb * 32;
 #pragma unroll
-  for (int c = 0; c < HD / 16; ++c) kr[c] = *(const uint4*)(krow + c * 16 + 8 * kh);
+  for (int tt = 0; tt < 2; ++tt) {
+    const int key = j0 + 16 * tt + r16 < n_keys ? j0 + 16 * tt + r16 : 0;
+    const uint16_t* krow = kbase + (size_t)key * HD;
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c) kr[tt * (HD / 32) + c] = *(const uint4*)(krow + c * 32 + 8 * g);
+  }
 #pragma unroll
   for (int it = 0; it < 32 * HD / 8 / AIO_WAVE; ++it) {
     const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
@@ -1037,7 +1050,7 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
   char* qs = smem;                  // [3][QR][QROW]; row kMaxRows of each term is zero
   char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the waves' states
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
-  const int rl = lane & 31, kh = lane >> 5;
+  const int col = lane & 15, g = lane >> 4;  // query column, lane group
   const int s = blockIdx.x, h = blockIdx.y, M = a.M;
   const int kvh = h / (a.H / a.Hkv);
   const int pos = a.st->pos;
@@ -1047,8 +1060,8 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
 
   const uint16_t* kbase = a.kc + (size_t)kvh * a.max_ctx * HD;
   const uint16_t* vbase = a.vc + (size_t)kvh * a.max_ctx * HD;
-  constexpr int NHB = HD / 32;           // 32-dim blocks of the output
-  constexpr int NKC = HD / 16;           // 16-dim chunks of a key row (per lane half)
+  constexpr int NDT = HD / 16;           // 16-dim tiles of the output
+  constexpr int NCH = HD / 32;           // 32-dim chunks of a key row
   constexpr int NVL = 32 * HD / 8 / AIO_WAVE;  // 16-byte value chunks per lane
   // The queries are requested first, then the wave's first key block:
   // loads complete in order, so waiting for the queries leaves the block in
@@ -1061,7 +1074,7 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
     const int e = tid + i * NT, qq = e / HD, dim = e % HD;
     qv[i] = e < M * HD ? a.q[(size_t)qq * a.H * HD + (size_t)h * HD + dim] : 0.f;
   }
-  uint4 kr[NKC], vr[NVL];
+  uint4 kr[2 * NCH], vr[NVL];
   int kb = kbA + wid;
   vattn_load<HD>(kbase, vbase, max(min(kb, kbB - 1), 0), n_keys, lane, kr, vr);
 
@@ -1081,17 +1094,17 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
     *(uint16_t*)(qs + ((e / HD) * Lds::QR + kMaxRows) * Lds::QROW + (e % HD) * 2) = 0;
   __syncthreads();
 
-  // this lane's query column rl: row rl sees keys [0, lim]
-  const bool live = rl < M;
-  const int lim = pos + (live ? rl : M - 1);
-  // lanes past the M rows read the zero row: their columns of S^T are zero
-  const char* qrow = qs + (live ? rl : kMaxRows) * Lds::QROW;
+  // this lane's query column col: row col sees keys [0, lim]
+  const bool live = col < M;
+  const int lim = pos + (live ? col : M - 1);
+  // columns past the M rows read the zero row: their columns of S^T are zero
+  const char* qrow = qs + (live ? col : kMaxRows) * Lds::QROW;
   char* vt = tail + wid * Lds::VBYTES;
-  f32x16 o[NHB];
+  f32x4 o[NDT];
 #pragma unroll
-  for (int hb = 0; hb < NHB; ++hb)
+  for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) o[hb][i] = 0.f;
+    for (int i = 0; i < 4; ++i) o[dt][i] = 0.f;
   float m = -INFINITY, lsum = 0.f;
 
   for (; kb < kbB; kb += kVAW) {
@@ -1104,19 +1117,35 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
       const u32x4 w = {vr[it].x, vr[it].y, vr[it].z, vr[it].w};
       *(u32x4*)(vt + kk * Lds::VROW + d0 * 2) = w;
     }
-    // scores S^T[key][query] over the HD dims, three query terms
-    f32x16 sc;
+    // scores S^T[key][query] over the HD dims, three query terms, two
+    // tiles of 16 keys.  The query fragments of chunk c + 1 are requested
+    // before the products of chunk c.
+    f32x4 sc[2];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-    for (int c = 0; c < NKC; ++c) {
-      const bf16x8 ak = as_bf16x8(kr[c]);
+      for (int i = 0; i < 4; ++i) sc[tt][i] = 0.f;
+    bf16x8 qf[2][3];
 #pragma unroll
-      for (int t = 0; t < 3; ++t) {
-        const bf16x8 bq = as_bf16x8(
-            *(const uint4*)(qrow + t * Lds::QR * Lds::QROW + (c * 16 + 8 * kh) * 2));
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq, sc, 0, 0, 0);
+    for (int t = 0; t < 3; ++t)
+      qf[0][t] = as_bf16x8(*(const uint4*)(qrow + t * Lds::QR * Lds::QROW + 8 * g * 2));
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      if (c + 1 < NCH) {
+#pragma unroll
+        for (int t = 0; t < 3; ++t)
+          qf[(c + 1) & 1][t] = as_bf16x8(
+              *(const uint4*)(qrow + t * Lds::QR * Lds::QROW + ((c + 1) * 32 + 8 * g) * 2));
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const bf16x8 ak = as_bf16x8(kr[tt * NCH + c]);
+#pragma unroll
+        for (int t = 0; t < 3; ++t)
+          sc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[c & 1][t], sc[tt], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     // the next block's keys and values are in flight during the softmax and
     // the P V product (the last block re-reads itself: no branch, so the
@@ -1124,78 +1153,80 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
     vattn_load<HD>(kbase, vbase, kb + kVAW < kbB ? kb + kVAW : kb, n_keys, lane, kr, vr);
     // causal mask (only a block holding keys past pos needs it; the test is
     // the same for the whole wave) and online softmax for this lane's query
+    // column; register j = 4 tt + v holds key j0 + vattn_key(g, j)
+    float sv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sv[j] = sc[j >> 2][j & 3];
     if (j0 + 31 > pos) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = j0 + 8 * (v / 4) + 4 * kh + (v % 4);
-        if (key > lim) sc[v] = -INFINITY;
-      }
+      for (int j = 0; j < 8; ++j)
+        if (j0 + vattn_key(g, j) > lim) sv[j] = -INFINITY;
     }
-    float mx = sc[0];
+    float mx = sv[0];
 #pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sc[v]);
+    for (int j = 1; j < 8; ++j) mx = fmaxf(mx, sv[j]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, AIO_WAVE));
     mx = fmaxf(mx, __shfl_xor(mx, 32, AIO_WAVE));
     const float mnew = fmaxf(m, mx);
     // while every key so far is masked, mnew is -inf: subtract 0 instead, so
     // exp2(-inf - 0) = 0 gives the zero weights (and o, lsum stay 0)
     const float mref = mnew == -INFINITY ? 0.f : mnew;
     const float cf = __builtin_amdgcn_exp2f(m - mref);
-    float p[16];
+    float p[8];
     float ps = 0.f;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      p[v] = __builtin_amdgcn_exp2f(sc[v] - mref);
-      ps += p[v];
+    for (int j = 0; j < 8; ++j) {
+      p[j] = __builtin_amdgcn_exp2f(sv[j] - mref);
+      ps += p[j];
     }
     lsum = lsum * cf + ps;
     m = mnew;
 #pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) o[hb][i] *= cf;
-    wave_lds_sync();  // the value tile is in LDS
-    // O^T += V^T P^T, two chunks of 16 keys, three terms of the weights.
-    // The weights split by truncation: t0 = the top 16 bits of p, t1 those
+      for (int i = 0; i < 4; ++i) o[dt][i] *= cf;
+    // the weights split by truncation: t0 = the top 16 bits of p, t1 those
     // of p - t0, t2 = p - t0 - t1 (exact: 8 significant bits each, 24 in
-    // all), without the rounding's branches.
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
+    // all), without the rounding's branches
+    bf16x8 bp[3];
+    {
       uint32_t tt[3][8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const uint32_t u0 = __float_as_uint(p[8 * c2 + e]) & 0xffff0000u;
-        const float r1 = p[8 * c2 + e] - __uint_as_float(u0);
+        const uint32_t u0 = __float_as_uint(p[e]) & 0xffff0000u;
+        const float r1 = p[e] - __uint_as_float(u0);
         const uint32_t u1 = __float_as_uint(r1) & 0xffff0000u;
         const float r2 = r1 - __uint_as_float(u1);
         tt[0][e] = u0;
         tt[1][e] = u1;
         tt[2][e] = __float_as_uint(r2);
       }
-      bf16x8 bp[3];
 #pragma unroll
       for (int t = 0; t < 3; ++t)
         bp[t] = as_bf16x8(make_uint4((tt[t][0] >> 16) | (tt[t][1] & 0xffff0000u),
                                      (tt[t][2] >> 16) | (tt[t][3] & 0xffff0000u),
                                      (tt[t][4] >> 16) | (tt[t][5] & 0xffff0000u),
                                      (tt[t][6] >> 16) | (tt[t][7] & 0xffff0000u)));
+    }
+    wave_lds_sync();  // the value tile is in LDS
+    // O^T += V^T P^T per 16-dim tile, three terms of the weights
 #pragma unroll
-      for (int hb = 0; hb < NHB; ++hb) {
-        // V^T fragment: dimension hb 32 + rl at this lane's eight keys
-        const char* vcol = vt + (hb * 32 + rl) * 2;
-        uint32_t w[4];
+    for (int dt = 0; dt < NDT; ++dt) {
+      // V^T fragment: dimension 16 dt + col at this lane group's eight keys
+      const char* vcol = vt + (dt * 16 + col) * 2;
+      uint32_t w[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          w[j] = (uint32_t)*(const uint16_t*)(vcol + vattn_key(c2, kh, 2 * j) * Lds::VROW) |
-                 ((uint32_t)*(const uint16_t*)(vcol + vattn_key(c2, kh, 2 * j + 1) * Lds::VROW)
-                  << 16);
-        const bf16x8 av = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+      for (int j = 0; j < 4; ++j)
+        w[j] = (uint32_t)*(const uint16_t*)(vcol + vattn_key(g, 2 * j) * Lds::VROW) |
+               ((uint32_t)*(const uint16_t*)(vcol + vattn_key(g, 2 * j + 1) * Lds::VROW) << 16);
+      const bf16x8 av = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
-          o[hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bp[t], o[hb], 0, 0, 0);
-      }
+      for (int t = 0; t < 3; ++t)
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bp[t], o[dt], 0, 0, 0);
     }
     wave_lds_sync();  // every read of the value tile is done before the next block's writes
   }
+  lsum += __shfl_xor(lsum, 16, AIO_WAVE);
   lsum += __shfl_xor(lsum, 32, AIO_WAVE);
 
   // every wave's state of the live rows -> LDS (over the value tiles)
@@ -1205,13 +1236,13 @@ __global__ __launch_bounds__(kVAW * AIO_WAVE, 1) void k_vattn_mma(VAttnArgs a) {
   float* ll = mm + kVAW * kMaxRows;            // [kVAW][kMaxRows] sum
   if (live) {
 #pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        om[(wid * kMaxRows + rl) * Lds::OROW + hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4)] = o[hb][v];
-    if (kh == 0) {
-      mm[wid * kMaxRows + rl] = m;
-      ll[wid * kMaxRows + rl] = lsum;
+      for (int v = 0; v < 4; ++v)
+        om[(wid * kMaxRows + col) * Lds::OROW + dt * 16 + 4 * g + v] = o[dt][v];
+    if (g == 0) {
+      mm[wid * kMaxRows + col] = m;
+      ll[wid * kMaxRows + col] = lsum;
     }
   }
   __syncthreads();
