@@ -1415,10 +1415,14 @@ hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits) 
     t.st = m.state();
     t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx; t.S = m.lay.splits; t.M = M;
     t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
-    // splits of kVattnBlocksPerWave key blocks per wave (the host's pos
-    // sizes the grid; the kernel takes its key range from the device state)
+    // splits of kVattnBlocksPerSplit key blocks, but no more workgroups than
+    // CUs: a workgroup takes a whole CU, and a second round of workgroups
+    // pays the queries' prologue and the merges again (at 32K, 64 splits per
+    // head cost 9.2 ms per 7B verify).  The host's pos sizes the grid; the
+    // kernel takes its key range from the device state.
     const int nkb = (pos + M + 31) / 32;
-    t.S = std::max(1, std::min(m.lay.vsplits, (nkb + kVattnBlocksPerSplit - 1) / kVattnBlocksPerSplit));
+    const int s_cap = std::max(1, std::min(m.lay.vsplits, m.num_cus / H));
+    t.S = std::max(1, std::min(s_cap, (nkb + kVattnBlocksPerSplit - 1) / kVattnBlocksPerSplit));
     t.cnt = m.at<int>(m.lay.vacnt);
     t.act = actB;
     t.lda = ka;

@@ -61,12 +61,13 @@ def test_fullsize_teacher_forced(name, n_steps):
         pair.close()
 
 
-@pytest.mark.parametrize("name", ["7b_int8", "7b", "1b"])
+@pytest.mark.parametrize("name", ["7b_int8", "7b", "1b", "7b_32k"])
 def test_verify_planted_3gram(name):
     """k = 8 verify of the planted 3-gram's drafts at the full shapes (the
     launch configuration the verify bench times): every row's logits and
     cache rows against the oracle from identical state, then the same
-    verify again, bit for bit."""
+    verify again, bit for bit.  At 32K positions the attention takes one
+    workgroup per CU, each wave streaming 16 key blocks."""
     cfg = synth.CONFIGS[name]
     pair = Pair(cfg)
     try:
