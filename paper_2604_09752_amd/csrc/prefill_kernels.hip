@@ -168,7 +168,7 @@ struct PGemmArgs {
   // tcnt[tile]; the last slice to arrive adds the partials in slice order
   // and runs the epilogue
   int ks;
-  float* fix;           // [tiles][ks][kGT threads][32]
+  float* fix;           // [tiles][ks][32][kGT threads]
   int* tcnt;            // [tiles], zero between products
 };
 
@@ -367,12 +367,14 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
     // K split: every slice's partial goes through memory (written through,
     // read past the caches); the last slice to arrive adds them in slice
     // order, so the sum is the same whatever the arrival order
+    // (element-major, so that each store and load instruction of a wave
+    // covers 256 contiguous bytes)
     const int tile = (int)(blockIdx.y * gridDim.x + blockIdx.x);
-    float* mine = a.fix + (((size_t)tile * a.ks + kz) * kGT + tid) * 32;
+    float* mine = a.fix + ((size_t)tile * a.ks + kz) * 32 * kGT + tid;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      st_agent(mine + v, ylo[v]);
-      st_agent(mine + 16 + v, yhi[v]);
+      st_agent(mine + v * kGT, ylo[v]);
+      st_agent(mine + (16 + v) * kGT, yhi[v]);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -384,12 +386,12 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) ylo[v] = yhi[v] = 0.f;
     for (int k = 0; k < a.ks; ++k) {
-      const float* pk = a.fix + (((size_t)tile * a.ks + k) * kGT + tid) * 32;
+      const float* pk = a.fix + ((size_t)tile * a.ks + k) * 32 * kGT + tid;
       float plo[16], phi[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        plo[v] = ld_agent(pk + v);
-        phi[v] = ld_agent(pk + 16 + v);
+        plo[v] = ld_agent(pk + v * kGT);
+        phi[v] = ld_agent(pk + (16 + v) * kGT);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -702,18 +704,17 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
   return hipGetLastError();
 }
 
-// Launch over `tiles` x (R / 64) tiles.  A residual product (O, down: d /
-// 128 tile columns) with fewer tiles than two per CU also splits K over
-// workgroups (up to kPfMaxKs slices of at least 8 stages), within the
-// fix-up buffer's room: 115 -> 85 us per product at 128 prompt rows.  The
-// QKV and gate/up products have 2-3x the tiles and lost more to the fix-up
-// (reading every slice's partial tile back) than they gained.
+// Launch over `tiles` x (R / 64) tiles.  A product with fewer tiles than
+// two per CU also splits K over workgroups (up to kPfMaxKs slices of at
+// least 8 stages), within the fix-up buffer's room: a workgroup streams its
+// stages one latency apart (about 0.9 us per 32-k stage), so at a short
+// prompt the 1B's QKV product (32 tiles of 64 stages) took 57 us alone.
 template <int WFMT, int EPI>
 hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g0, int tiles) {
   PGemmArgs g = g0;
   const int rt = (g.R + kBR - 1) / kBR, nst = g.K / kKT;
   g.ks = 1;
-  while (EPI == PE_RESID && tiles * rt * g.ks < 2 * m.num_cus && 2 * g.ks <= kPfMaxKs &&
+  while (tiles * rt * g.ks < 2 * m.num_cus && 2 * g.ks <= kPfMaxKs &&
          nst / (2 * g.ks) >= 8 &&
          (size_t)tiles * rt * 2 * g.ks * kGT * 32 * 4 <= m.lay.pfix_bytes &&
          (size_t)tiles * rt <= m.lay.pcnt_n)

@@ -33,6 +33,12 @@ CASES = {
     # head_dim 128 with 4 query heads per kv head
     "hd128_gqa4": (dict(n_heads=4, n_kv_heads=1, head_dim=128), 0, 100),
     "int8": (dict(wfmt="int8"), 0, 23),
+    # d 1024, FFN 4096: at a short prompt every product (QKV and gate/up as
+    # well as O and down) has fewer tiles than two per CU and splits K over
+    # workgroups, the last slice adding the partial tiles in slice order
+    "split_k": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128), 0, 10),
+    "split_k_int8": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
+                          wfmt="int8"), 0, 70),
 }
 
 
