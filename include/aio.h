@@ -315,7 +315,9 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
  * rows per pass over the weights) with causal attention, writes every
  * token's K/V in every layer, and writes the logits after the last token,
  * fp32 [vocab], to logits_dev (16-byte aligned).  The result equals n
- * aio_decode_step calls up to rounding.  The scratch
+ * aio_decode_step calls up to rounding.  A prompt of at most max_verify
+ * tokens goes through the verify forward instead (the same kernels as
+ * aio_verify; no scratch beyond the workspace).  The scratch
  * (4 (1 + d + H hd + max(d, H hd) + F) bytes per row, for up to 2048 rows) is allocated by
  * the library on the first call that needs more and kept until
  * aio_model_free, so such a call synchronises once.  Asynchronous
@@ -337,14 +339,17 @@ int aio_prefill(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos, flo
  * aio_prefill_noalloc_rows(cfg) rows (the array divided by the scratch of
  * one row: 4 (1 + d + H hd + max(d, H hd) + F) bytes, and at most 2048),
  * so any n works; results equal aio_prefill's up to rounding (bit-identical
- * where both take the prompt in one pass).  Every GPU holds one such array
+ * where both take the prompt in one pass; a prompt of at most max_verify
+ * tokens takes aio_prefill's verify route and needs none of the array).
+ * Every GPU holds one such array
  * for the whole process, shared by all calls on that GPU: calls that
  * overlap on one GPU (handles on different streams) race and must be
  * serialised by the caller.  Nothing in the array needs to start at zero:
  * each call writes every region before reading it.  Asynchronous like
  * aio_verify; the tokens are copied from host memory on the model's stream.
- * Errors as aio_prefill, and AIO_EUNSUPPORTED when one row's scratch
- * exceeds the array (aio_prefill_noalloc_rows(cfg) == 0). */
+ * Errors as aio_prefill, and AIO_EUNSUPPORTED when a prompt of more than
+ * max_verify tokens meets a config whose one row's scratch exceeds the
+ * array (aio_prefill_noalloc_rows(cfg) == 0). */
 int aio_prefill_noalloc(aio_model* m, const int32_t* tokens, int32_t n, int32_t pos,
                         float* logits_dev);
 

@@ -132,7 +132,11 @@ hipError_t aio_launch_argmax(const aio_model& m, const float* logits, int rows, 
                              int32_t* out, bool greedy_feedback);
 
 // ---- launchers (verify_kernels.hip) ----
-hipError_t aio_launch_verify(const aio_model& m, int rows, int pos, float* logits);
+// The verify forward of the rows set by aio_launch_set_rows at pos .. pos +
+// rows - 1: their K/V in every layer and logits [rows][vocab], or with
+// last_row_only the last row's logits [vocab] only.
+hipError_t aio_launch_verify(const aio_model& m, int rows, int pos, float* logits,
+                             bool last_row_only = false);
 // Final RMSNorm and LM head of the first `rows` rows of the workspace's
 // residual rows (lay.x): logits [rows][vocab].
 hipError_t aio_launch_lm_rows(const aio_model& m, int rows, float* logits);

@@ -1381,7 +1381,8 @@ hipError_t launch_vattn_mma(const aio_model& m, const VAttnArgs& t) {
 
 }  // namespace
 
-hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits) {
+hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits,
+                             bool last_row_only) {
   const aio_config& c = m.cfg;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int ka = m.lay.ka;
@@ -1449,6 +1450,13 @@ hipError_t aio_launch_verify(const aio_model& m, int M, int pos, float* logits) 
     dn.N = d; dn.K = F; dn.out = x; dn.ldo = d; dn.st = m.state();
     dn.g_next = (const uint16_t*)g_after; dn.act_next = actA;
     if ((e = launch_vgemm<EPI_RESID>(m, dn, d / 64)) != hipSuccess) return e;
+  }
+  if (last_row_only) {
+    // the last row's final RMSNorm and LM head only (a prefill of M tokens)
+    if (M > 1 && (e = hipMemcpyAsync(x, x + (size_t)(M - 1) * d, (size_t)d * sizeof(float),
+                                     hipMemcpyDeviceToDevice, m.stream)) != hipSuccess)
+      return e;
+    return aio_launch_lm_rows(m, 1, logits);
   }
   VGemmArgs lm{};
   lm.act = actA; lm.lda = ka; lm.M = M;

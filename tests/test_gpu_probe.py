@@ -21,6 +21,7 @@ TINY = synth.CONFIGS["tiny"]
 CASES = {
     # name: (config changes, tokens already in the cache, prompt tokens)
     "n1": (dict(), 0, 1),
+    # up to max_verify (10) tokens the prefill is the verify forward
     "n10": (dict(), 0, 10),
     "n23": (dict(), 0, 23),
     "n128": (dict(), 0, 128),
@@ -36,7 +37,7 @@ CASES = {
     # d 1024, FFN 4096: at a short prompt every product (QKV and gate/up as
     # well as O and down) has fewer tiles than two per CU and splits K over
     # workgroups, the last slice adding the partial tiles in slice order
-    "split_k": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128), 0, 10),
+    "split_k": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128), 0, 23),
     "split_k_int8": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
                           wfmt="int8"), 0, 70),
 }
