@@ -241,10 +241,13 @@ AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const 
 template <int WFMT, int A_LD>
 AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[kBLd],
                           const uint4 (&ra)[A_LD], const uint4 (&rb)[kBLd]) {
+  // (vector stores: a uint4 struct copy is a memcpy, which keeps the
+  // register sets in scratch memory)
 #pragma unroll
   for (int j = 0; j < A_LD; ++j) {
     if constexpr (WFMT == AIO_WFMT_BF16) {
-      *(uint4*)(buf + alds[j]) = ra[j];
+      const u32x4 w = {ra[j].x, ra[j].y, ra[j].z, ra[j].w};
+      *(u32x4*)(buf + alds[j]) = w;
     } else {
       const uint32_t w[4] = {ra[j].x, ra[j].y, ra[j].z, ra[j].w};
       uint32_t o[8];
@@ -255,12 +258,16 @@ AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[
         const float f0 = (float)(int8_t)(sw >> sh), f1 = (float)(int8_t)(sw >> (sh + 8));
         o[i] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xffff0000u);
       }
-      *(uint4*)(buf + alds[j]) = make_uint4(o[0], o[1], o[2], o[3]);
-      *(uint4*)(buf + alds[j] + 16) = make_uint4(o[4], o[5], o[6], o[7]);
+      const u32x4 w0 = {o[0], o[1], o[2], o[3]}, w1 = {o[4], o[5], o[6], o[7]};
+      *(u32x4*)(buf + alds[j]) = w0;
+      *(u32x4*)(buf + alds[j] + 16) = w1;
     }
   }
 #pragma unroll
-  for (int j = 0; j < kBLd; ++j) *(uint4*)(buf + blds[j]) = rb[j];
+  for (int j = 0; j < kBLd; ++j) {
+    const u32x4 w = {rb[j].x, rb[j].y, rb[j].z, rb[j].w};
+    *(u32x4*)(buf + blds[j]) = w;
+  }
 }
 
 // The MFMA products of one LDS stage: 16-k chunks, the wave's two row blocks
@@ -333,21 +340,41 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[b][t][i] = 0.f;
 
-  // this workgroup's stages [sA, sB) of K (all of them unless K is split)
+  // this workgroup's stages [sA, sB) of K (all of them unless K is split).
+  // Two register sets keep two stages' loads in flight (a stage's loads take
+  // a memory round trip, its products a fraction of one): set 1 holds the
+  // stages sA + 1, sA + 3, ..., set 0 the others; loads past sB re-read the
+  // last stage and are not used.
   const int nst = a.K / kKT, kz = (int)blockIdx.z;
   const int sA = kz * nst / a.ks, sB = (kz + 1) * nst / a.ks;
+  uint4 ra1[A_LD], rb1[kBLd];
+  const int sL = sB - 1;
   gload_stage<WFMT, A_LD>(aptr, bptr, sA, ra_, rb_);
+  gload_stage<WFMT, A_LD>(aptr, bptr, min(sA + 1, sL), ra1, rb1);
   lstore_stage<WFMT, A_LD>(smem, alds, blds, ra_, rb_);
   __syncthreads();
-  // every stage but the last: the next stage's loads are in flight while the
-  // current one is multiplied, then go to the other buffer
-  for (int st = sA; st + 1 < sB; ++st) {
-    gload_stage<WFMT, A_LD>(aptr, bptr, st + 1, ra_, rb_);
-    stage_product(smem + ((st - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
-    lstore_stage<WFMT, A_LD>(smem + ((st + 1 - sA) & 1) * kStageB, alds, blds, ra_, rb_);
-    __syncthreads();
+  gload_stage<WFMT, A_LD>(aptr, bptr, min(sA + 2, sL), ra_, rb_);
+  // stage S from its LDS buffer; then stage S + 1 (in set RA, RB) to the
+  // other buffer, and the set refilled with stage S + 3 (written out for
+  // each set: a set chosen at run time would live in scratch memory)
+#define AIO_PF_STEP(S, RA, RB)                                                          \
+  do {                                                                                 \
+    stage_product(smem + (((S) - sA) & 1) * kStageB, wn, wr, rl, kh, acc);             \
+    lstore_stage<WFMT, A_LD>(smem + (((S) + 1 - sA) & 1) * kStageB, alds, blds, RA, RB); \
+    __syncthreads();                                                                   \
+    gload_stage<WFMT, A_LD>(aptr, bptr, min((S) + 3, sL), RA, RB);                     \
+  } while (0)
+  int st = sA;
+  for (; st + 2 < sB; st += 2) {
+    AIO_PF_STEP(st, ra1, rb1);
+    AIO_PF_STEP(st + 1, ra_, rb_);
   }
-  stage_product(smem + ((sB - 1 - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
+  if (st + 1 < sB) {
+    AIO_PF_STEP(st, ra1, rb1);
+    ++st;
+  }
+#undef AIO_PF_STEP
+  stage_product(smem + ((st - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
 
   // the tile's sums over the three terms: lane l, register v -> column
   // (prompt row) l % 32, row i = 8 (v / 4) + 4 (l / 32) + v % 4 of the
