@@ -119,26 +119,38 @@ __global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
 
 // --------------------------------------------------------------------- GEMM
 
-// A workgroup of 4 waves computes a tile of 128 weight rows (4 blocks of
-// 32) by 64 prompt rows, every term of each.  Wave (wn, wr) owns row blocks
-// 2 wn ("lo") and 2 wn + 1 ("hi") and prompt rows [32 wr, 32 wr + 32), so the
-// two rows an epilogue combines (a RoPE pair, gate and up) sit in one lane.
+// A workgroup of 2 WN waves computes a tile of 64 WN weight rows (2 WN
+// blocks of 32, in "units" of 128 rows, the granule of the row mapping
+// below) by 64 prompt rows, every term of each.  Wave (wn, wr) owns row
+// blocks 2 wn ("lo") and 2 wn + 1 ("hi") and prompt rows [32 wr, 32 wr +
+// 32), so the two rows an epilogue combines (a RoPE pair, gate and up) sit
+// in one lane.  Long prompts take WN = 4 (256 rows): the loads, not the
+// MFMAs, set the rate, and the larger tile does twice the products for 1.4x
+// the bytes per stage (prefill of 2048 tokens 32.2 -> 28.5 ms); short ones
+// WN = 2, which gives twice the workgroups.
 // Weights and activations pass through LDS in stages of 32 k, double
 // buffered: the next stage's global loads are in flight in registers while
 // the current one is multiplied.  Rows in LDS are 80 bytes apart (64 + a
 // 16-byte skew), so the 32 rows a fragment read touches spread over the
 // banks.
-constexpr int kGT = 256;
 constexpr int kPfMaxKs = 8;  // most K slices of a prefill product
-constexpr int kBM = 128;  // weight rows per tile
+constexpr int kUnit = 128;   // weight rows per unit of the row mapping (block_src)
 constexpr int kBR = 64;   // prompt rows per tile
 constexpr int kKT = 32;   // k per stage
 constexpr int kRowB = kKT * 2 + 16;
 constexpr int kBCols = kNT * kBR;                  // activation columns: term-major per wave half
-constexpr int kStageB = (kBM + kBCols) * kRowB;    // weight rows + activation columns
-constexpr int kGemmLds = 2 * kStageB;
-constexpr int kBLd = kBCols * (kKT / 8) / kGT;     // 16-byte activation loads per thread
-static_assert(kBCols * (kKT / 8) % kGT == 0, "activation stage must split evenly");
+constexpr int kBChunks = kBCols * (kKT / 8);       // 16-byte activation chunks per stage
+
+// The tile shape of WN waves across the weight rows.
+template <int WN>
+struct PTile {
+  static constexpr int GT = 2 * WN * AIO_WAVE;              // threads
+  static constexpr int BM = 64 * WN;                        // weight rows
+  static constexpr int UPT = BM / kUnit;                    // units per tile
+  static constexpr int BLd = (kBChunks + GT - 1) / GT;      // activation loads per thread
+  static constexpr int StageB = (BM + kBCols) * kRowB;      // weight rows + activation columns
+  static constexpr int Lds = 2 * StageB;
+};
 
 enum PEpi { PE_QKV = 0, PE_RESID = 1, PE_SWIGLU = 2 };
 
@@ -168,11 +180,11 @@ struct PGemmArgs {
   // tcnt[tile]; the last slice to arrive adds the partials in slice order
   // and runs the epilogue
   int ks;
-  float* fix;           // [tiles][ks][32][kGT threads]
+  float* fix;           // [tiles][ks][32][threads]
   int* tcnt;            // [tiles], zero between products
 };
 
-// Where block `blk` (0..3) of tile `bx` reads its 32 rows: matrix index
+// Where block `blk` (0..3) of unit `bx` reads its 32 rows: matrix index
 // (0, 1, 2 = w0, w1, w2), first row in that matrix, and the number of valid
 // rows (0 for a block past the end).
 struct BlockSrc {
@@ -208,7 +220,7 @@ AIO_DEV BlockSrc block_src(const PGemmArgs& a, int bx, int blk) {
     b.row0 = f;
     b.valid = f < a.N ? min(32, a.N - f) : 0;
   } else {
-    const int n = bx * kBM + blk * 32;
+    const int n = bx * kUnit + blk * 32;
     b.row0 = n;
     b.valid = n < a.N ? min(32, a.N - n) : 0;
   }
@@ -223,24 +235,28 @@ AIO_DEV const char* pick_mat(const PGemmArgs& a, int mat) {
   return (const char*)(b0 + (uint64_t)(mat == 1) * d1 + (uint64_t)(mat == 2) * d2);
 }
 
-// Global loads of stage st: A_LD 16-byte weight chunks and kBLd activation
+// Global loads of stage st: A_LD 16-byte weight chunks and BLD activation
 // chunks per thread.
-template <int WFMT, int A_LD>
-AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const (&bptr)[kBLd],
-                         int st, uint4 (&ra)[A_LD], uint4 (&rb)[kBLd]) {
+template <int WFMT, int WN, int A_LD, int BLD = PTile<WN>::BLd>
+AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const (&bptr)[BLD],
+                         int st, uint4 (&ra)[A_LD], uint4 (&rb)[BLD]) {
+  constexpr int GT = PTile<WN>::GT;
   constexpr int wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
   const size_t ko = (size_t)st * kKT;
 #pragma unroll
   for (int j = 0; j < A_LD; ++j) ra[j] = ld_stream((const uint4*)(aptr[j] + ko * wbytes));
 #pragma unroll
-  for (int j = 0; j < kBLd; ++j) rb[j] = *(const uint4*)(bptr[j] + ko);
+  for (int j = 0; j < BLD; ++j)
+    if (j + 1 < BLD || kBChunks % GT == 0 || (int)threadIdx.x < kBChunks % GT)
+      rb[j] = *(const uint4*)(bptr[j] + ko);
 }
 
 // The same chunks into an LDS stage buffer (int8 widened to bf16, exact:
 // |q| <= 127).
-template <int WFMT, int A_LD>
-AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[kBLd],
-                          const uint4 (&ra)[A_LD], const uint4 (&rb)[kBLd]) {
+template <int WFMT, int WN, int A_LD, int BLD = PTile<WN>::BLd>
+AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[BLD],
+                          const uint4 (&ra)[A_LD], const uint4 (&rb)[BLD]) {
+  constexpr int GT = PTile<WN>::GT;
   // (vector stores: a uint4 struct copy is a memcpy, which keeps the
   // register sets in scratch memory)
 #pragma unroll
@@ -264,17 +280,20 @@ AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[
     }
   }
 #pragma unroll
-  for (int j = 0; j < kBLd; ++j) {
-    const u32x4 w = {rb[j].x, rb[j].y, rb[j].z, rb[j].w};
-    *(u32x4*)(buf + blds[j]) = w;
-  }
+  for (int j = 0; j < BLD; ++j)
+    if (j + 1 < BLD || kBChunks % GT == 0 || (int)threadIdx.x < kBChunks % GT) {
+      const u32x4 w = {rb[j].x, rb[j].y, rb[j].z, rb[j].w};
+      *(u32x4*)(buf + blds[j]) = w;
+    }
 }
 
 // The MFMA products of one LDS stage: 16-k chunks, the wave's two row blocks
 // by the terms of its 32 prompt rows.  Activation columns of the stage are
 // ordered [wave half wr][term][row].
+template <int WN>
 AIO_DEV void stage_product(const char* cur, int wn, int wr, int rl, int kh,
                            f32x16 (&acc)[2][kNT]) {
+  constexpr int kBM = PTile<WN>::BM;
 #pragma unroll
   for (int c16 = 0; c16 < kKT / 16; ++c16) {
     const int koff = (c16 * 16 + 8 * kh) * 2;
@@ -293,11 +312,13 @@ AIO_DEV void stage_product(const char* cur, int wn, int wr, int rl, int kh,
   }
 }
 
-template <int WFMT, int EPI>
-__global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
+template <int WFMT, int EPI, int WN>
+__global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
+  using Tl = PTile<WN>;
+  constexpr int kGT = Tl::GT, kBM = Tl::BM, kBLd = Tl::BLd, kStageB = Tl::StageB;
   extern __shared__ __align__(16) char smem[];
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
-  const int wn = wid & 1, wr = wid >> 1;
+  const int wn = wid % WN, wr = wid / WN;
   const int rl = lane & 31, kh = lane >> 5;
   const int bx = blockIdx.x, r0 = blockIdx.y * kBR;
   constexpr int wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
@@ -314,7 +335,8 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
 #pragma unroll
   for (int j = 0; j < A_LD; ++j) {
     const int f = j * kGT + tid, ra = f / A_CPR, ca = f % A_CPR;
-    const BlockSrc s = block_src<EPI>(a, bx, ra >> 5);
+    const int blk = ra >> 5;  // block of the tile: unit UPT bx + blk / 4, block blk % 4 of it
+    const BlockSrc s = block_src<EPI>(a, Tl::UPT * bx + (blk >> 2), blk & 3);
     int row = s.row0 + ((ra & 31) < s.valid ? (ra & 31) : 0);
     if (s.valid == 0) row = 0;  // a block past the end reads row 0 of w0 (discarded)
     const char* w = s.valid ? pick_mat(a, s.mat) : (const char*)a.w0;
@@ -325,7 +347,7 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
   int blds[kBLd];
 #pragma unroll
   for (int j = 0; j < kBLd; ++j) {
-    const int f = j * kGT + tid, cb = f / 4, c = f % 4;
+    const int f = min(j * kGT + tid, kBChunks - 1), cb = f / 4, c = f % 4;
     const int half = cb / (kNT * 32), t = (cb / 32) % kNT;
     const int row = r0 + half * 32 + (cb & 31);
     bptr[j] = a.act + t * a.tstride + (size_t)(row < a.R ? row : a.R - 1) * a.lda + c * 8;
@@ -349,20 +371,20 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
   const int sA = kz * nst / a.ks, sB = (kz + 1) * nst / a.ks;
   uint4 ra1[A_LD], rb1[kBLd];
   const int sL = sB - 1;
-  gload_stage<WFMT, A_LD>(aptr, bptr, sA, ra_, rb_);
-  gload_stage<WFMT, A_LD>(aptr, bptr, min(sA + 1, sL), ra1, rb1);
-  lstore_stage<WFMT, A_LD>(smem, alds, blds, ra_, rb_);
+  gload_stage<WFMT, WN, A_LD>(aptr, bptr, sA, ra_, rb_);
+  gload_stage<WFMT, WN, A_LD>(aptr, bptr, min(sA + 1, sL), ra1, rb1);
+  lstore_stage<WFMT, WN, A_LD>(smem, alds, blds, ra_, rb_);
   __syncthreads();
-  gload_stage<WFMT, A_LD>(aptr, bptr, min(sA + 2, sL), ra_, rb_);
+  gload_stage<WFMT, WN, A_LD>(aptr, bptr, min(sA + 2, sL), ra_, rb_);
   // stage S from its LDS buffer; then stage S + 1 (in set RA, RB) to the
   // other buffer, and the set refilled with stage S + 3 (written out for
   // each set: a set chosen at run time would live in scratch memory)
 #define AIO_PF_STEP(S, RA, RB)                                                          \
   do {                                                                                 \
-    stage_product(smem + (((S) - sA) & 1) * kStageB, wn, wr, rl, kh, acc);             \
-    lstore_stage<WFMT, A_LD>(smem + (((S) + 1 - sA) & 1) * kStageB, alds, blds, RA, RB); \
+    stage_product<WN>(smem + (((S) - sA) & 1) * kStageB, wn, wr, rl, kh, acc);             \
+    lstore_stage<WFMT, WN, A_LD>(smem + (((S) + 1 - sA) & 1) * kStageB, alds, blds, RA, RB); \
     __syncthreads();                                                                   \
-    gload_stage<WFMT, A_LD>(aptr, bptr, min((S) + 3, sL), RA, RB);                     \
+    gload_stage<WFMT, WN, A_LD>(aptr, bptr, min((S) + 3, sL), RA, RB);                     \
   } while (0)
   int st = sA;
   for (; st + 2 < sB; st += 2) {
@@ -374,7 +396,7 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
     ++st;
   }
 #undef AIO_PF_STEP
-  stage_product(smem + ((st - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
+  stage_product<WN>(smem + ((st - sA) & 1) * kStageB, wn, wr, rl, kh, acc);
 
   // the tile's sums over the three terms: lane l, register v -> column
   // (prompt row) l % 32, row i = 8 (v / 4) + 4 (l / 32) + v % 4 of the
@@ -431,8 +453,8 @@ __global__ __launch_bounds__(kGT) void k_pgemm(PGemmArgs a) {
   // Epilogue.
   const int r = r0 + wr * 32 + rl;
   if (r >= a.R) return;
-  const BlockSrc slo = block_src<EPI>(a, bx, 2 * wn);
-  const BlockSrc shi = block_src<EPI>(a, bx, 2 * wn + 1);
+  const BlockSrc slo = block_src<EPI>(a, Tl::UPT * bx + (wn >> 1), 2 * (wn & 1));
+  const BlockSrc shi = block_src<EPI>(a, Tl::UPT * bx + (wn >> 1), 2 * (wn & 1) + 1);
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int i = 8 * (v / 4) + 4 * kh + (v % 4);
@@ -731,34 +753,47 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
   return hipGetLastError();
 }
 
-// Launch over `tiles` x (R / 64) tiles.  A product with fewer tiles than
-// two per CU also splits K over workgroups (up to kPfMaxKs slices of at
-// least 8 stages), within the fix-up buffer's room: a workgroup streams its
-// stages one latency apart (about 0.9 us per 32-k stage), so at a short
-// prompt the 1B's QKV product (32 tiles of 64 stages) took 57 us alone.
-template <int WFMT, int EPI>
-hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g0, int tiles) {
+// Launch over `units` (of 128 weight rows) x (R / 64) prompt-row tiles,
+// in tiles of WN / 2 units.  A product with fewer tiles than two per CU
+// also splits K over workgroups (up to kPfMaxKs slices of at least 8
+// stages), within the fix-up buffer's room: a workgroup streams its stages
+// one latency apart, so at a short prompt the 1B's QKV product (32 tiles of
+// 64 stages) took 57 us unsplit.
+template <int WFMT, int EPI, int WN>
+hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g0, int units) {
+  using Tl = PTile<WN>;
   PGemmArgs g = g0;
+  const int tiles = (units + Tl::UPT - 1) / Tl::UPT;
   const int rt = (g.R + kBR - 1) / kBR, nst = g.K / kKT;
   g.ks = 1;
   while (tiles * rt * g.ks < 2 * m.num_cus && 2 * g.ks <= kPfMaxKs &&
          nst / (2 * g.ks) >= 8 &&
-         (size_t)tiles * rt * 2 * g.ks * kGT * 32 * 4 <= m.lay.pfix_bytes &&
+         (size_t)tiles * rt * 2 * g.ks * Tl::GT * 32 * 4 <= m.lay.pfix_bytes &&
          (size_t)tiles * rt <= m.lay.pcnt_n)
     g.ks *= 2;
   g.fix = m.at<float>(m.lay.pfix);
   g.tcnt = m.at<int>(m.lay.pcnt);
-  const void* fn = (const void*)k_pgemm<WFMT, EPI>;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+  const void* fn = (const void*)k_pgemm<WFMT, EPI, WN>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, Tl::Lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_pgemm<WFMT, EPI>), dim3(tiles, rt, g.ks), dim3(kGT), kGemmLds, m.stream, g);
+  hipLaunchKernelGGL((k_pgemm<WFMT, EPI, WN>), dim3(tiles, rt, g.ks), dim3(Tl::GT), Tl::Lds,
+                     m.stream, g);
   return hipGetLastError();
 }
 
+// 256-row tiles from 16 prompt-row tiles (1024 rows) on, 128-row tiles
+// below (at 512 rows the smaller tiles were still ahead: 8.76 against
+// 8.99 ms for the 1B).
+template <int WFMT, int EPI>
+hipError_t launch_pgemm_w(const aio_model& m, const PGemmArgs& g, int units) {
+  if ((g.R + kBR - 1) / kBR >= 16) return launch_pgemm_t<WFMT, EPI, 4>(m, g, units);
+  return launch_pgemm_t<WFMT, EPI, 2>(m, g, units);
+}
+
 template <int EPI>
-hipError_t launch_pgemm(const aio_model& m, const PGemmArgs& g, int tiles) {
-  if (m.cfg.wfmt == AIO_WFMT_INT8) return launch_pgemm_t<AIO_WFMT_INT8, EPI>(m, g, tiles);
-  return launch_pgemm_t<AIO_WFMT_BF16, EPI>(m, g, tiles);
+hipError_t launch_pgemm(const aio_model& m, const PGemmArgs& g, int units) {
+  if (m.cfg.wfmt == AIO_WFMT_INT8) return launch_pgemm_w<AIO_WFMT_INT8, EPI>(m, g, units);
+  return launch_pgemm_w<AIO_WFMT_BF16, EPI>(m, g, units);
 }
 
 template <int HD>
@@ -836,7 +871,7 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     o.act = b.actA; o.lda = b.lda_a; o.tstride = tsA; o.R = R;
     o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
     o.N = d; o.K = H * hd; o.out = b.x; o.ldo = d;
-    if ((e = launch_pgemm<PE_RESID>(m, o, (d + kBM - 1) / kBM)) != hipSuccess) return e;
+    if ((e = launch_pgemm<PE_RESID>(m, o, (d + kUnit - 1) / kUnit)) != hipSuccess) return e;
 
     if ((e = launch_pnorm(m, b, R, nullptr, L.ffn_norm)) != hipSuccess) return e;
     PGemmArgs gu{};
@@ -851,7 +886,7 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     dn.act = b.actB; dn.lda = b.lda_b; dn.tstride = tsB; dn.R = R;
     dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
     dn.N = d; dn.K = F; dn.out = b.x; dn.ldo = d;
-    if ((e = launch_pgemm<PE_RESID>(m, dn, (d + kBM - 1) / kBM)) != hipSuccess) return e;
+    if ((e = launch_pgemm<PE_RESID>(m, dn, (d + kUnit - 1) / kUnit)) != hipSuccess) return e;
   }
   return hipSuccess;
 }

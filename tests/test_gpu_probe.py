@@ -40,6 +40,10 @@ CASES = {
     "split_k": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128), 0, 23),
     "split_k_int8": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
                           wfmt="int8"), 0, 70),
+    # 1100 prompt rows (18 tiles of 64): 256-row weight tiles of 8 waves, K
+    # still split in two for QKV and O
+    "wide_tiles": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
+                        prompt_len=1100), 0, 1100),
 }
 
 
