@@ -563,7 +563,9 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
   char* tail = smem + Lds::QBYTES;  // per wave: value tile; at the end: the merge
   const int tid = threadIdx.x, lane = tid & (AIO_WAVE - 1), wid = tid / AIO_WAVE;
   const int rl = lane & 31, kh = lane >> 5;
-  const int q0 = blockIdx.x * 32, h = blockIdx.y;
+  // query tiles in reverse: a causal tile's work grows with its position,
+  // and workgroups start in index order, so the longest start first
+  const int q0 = (int)(gridDim.x - 1 - blockIdx.x) * 32, h = blockIdx.y;
   const int G = a.H / a.Hkv, kvh = h / G;
   const int rows = min(32, a.R - q0);
   const int n_keys = a.pos0 + q0 + rows;  // keys the block's last row sees
@@ -597,37 +599,54 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
     for (int i = 0; i < 16; ++i) o[hb][i] = 0.f;
   float m = -INFINITY, lsum = 0.f;
 
+  // Block kb's key fragments (A operand: key row rl, dims 16 c + 8 kh ..) and
+  // value chunks (16 bytes of 8 dims, row-major) into registers; keys past
+  // n_keys read key 0.  The next block of the wave is requested while the
+  // current one is multiplied.
+  constexpr int NKC = HD / 16, VCH = 32 * HD / 8, NVL = VCH / AIO_WAVE;
+  uint4 kr[NKC], vr[NVL];
+  auto load_block = [&](int kb) {
+    const int j0 = kb * 32;
+    const int key = j0 + rl < n_keys ? j0 + rl : 0;
+    const uint16_t* krow = kbase + (size_t)key * HD;
+#pragma unroll
+    for (int c = 0; c < NKC; ++c) kr[c] = *(const uint4*)(krow + c * 16 + 8 * kh);
+#pragma unroll
+    for (int it = 0; it < NVL; ++it) {
+      const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
+      const int vkey = j0 + kk < n_keys ? j0 + kk : 0;
+      vr[it] = *(const uint4*)(vbase + (size_t)vkey * HD + d0);
+    }
+  };
+  if (wid < nkb) load_block(wid);
+
   for (int kb = wid; kb < nkb; kb += kAW) {
     const int j0 = kb * 32;
-    // value rows -> LDS, row by row (16-byte chunks of 8 dims; a vector
-    // store: a uint4 struct copy would go through scratch memory)
-    constexpr int VCH = 32 * HD / 8;
+    // value rows -> LDS, row by row (a vector store: a uint4 struct copy
+    // would go through scratch memory)
 #pragma unroll
-    for (int it = 0; it < VCH / AIO_WAVE; ++it) {
+    for (int it = 0; it < NVL; ++it) {
       const int f = it * AIO_WAVE + lane, kk = f / (HD / 8), d0 = (f % (HD / 8)) * 8;
-      const int key = j0 + kk < n_keys ? j0 + kk : 0;
-      const uint4 w = *(const uint4*)(vbase + (size_t)key * HD + d0);
-      const u32x4 wv = {w.x, w.y, w.z, w.w};
+      const u32x4 wv = {vr[it].x, vr[it].y, vr[it].z, vr[it].w};
       *(u32x4*)(vt + kk * Lds::VROW + d0 * 2) = wv;
     }
     // scores: S^T[key i][query j] over the HD dims, three query terms
     f32x16 s;
 #pragma unroll
     for (int i = 0; i < 16; ++i) s[i] = 0.f;
-    {
-      const int key = j0 + rl < n_keys ? j0 + rl : 0;
-      const uint16_t* krow = kbase + (size_t)key * HD;
 #pragma unroll
-      for (int c = 0; c < HD / 16; ++c) {
-        const bf16x8 ak = as_bf16x8(*(const uint4*)(krow + c * 16 + 8 * kh));
+    for (int c = 0; c < NKC; ++c) {
+      const bf16x8 ak = as_bf16x8(kr[c]);
 #pragma unroll
-        for (int t = 0; t < 3; ++t) {
-          const bf16x8 bq =
-              as_bf16x8(*(const uint4*)(qs + (t * 32 + rl) * Lds::QROW + (c * 16 + 8 * kh) * 2));
-          s = mfma(ak, bq, s);
-        }
+      for (int t = 0; t < 3; ++t) {
+        const bf16x8 bq =
+            as_bf16x8(*(const uint4*)(qs + (t * 32 + rl) * Lds::QROW + (c * 16 + 8 * kh) * 2));
+        s = mfma(ak, bq, s);
       }
     }
+    // the wave's next block (the last one re-reads itself: no branch, so
+    // the fragments stay in registers)
+    load_block(kb + kAW < nkb ? kb + kAW : kb);
     // causal mask and online softmax for this lane's query (column rl)
     float mx = -INFINITY;
 #pragma unroll
@@ -638,12 +657,15 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
     }
     mx = fmaxf(mx, __shfl_xor(mx, 32, AIO_WAVE));
     const float mnew = fmaxf(m, mx);
-    const float c = (m == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : exp2f(m - mnew);
+    // (the hardware exp2: every argument is <= 0, and exp2(-inf) = 0)
+    const float c =
+        (m == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : __builtin_amdgcn_exp2f(m - mnew);
+    const float mref = mnew == -INFINITY ? 0.f : mnew;
     float p[16];
     float ps = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      p[v] = s[v] == -INFINITY ? 0.f : exp2f(s[v] - mnew);
+      p[v] = __builtin_amdgcn_exp2f(s[v] - mref);
       ps += p[v];
     }
     lsum = lsum * c + ps;
@@ -656,16 +678,25 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
     // O^T += V^T P^T, two chunks of 16 keys, three terms of the weights
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
-      uint16_t tt[3][8];
+      // the weights split by truncation: t0 = the top 16 bits of p, t1 those
+      // of p - t0, t2 = p - t0 - t1 (exact: 8 significant bits each)
+      uint32_t tt[3][8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) split3(p[8 * c2 + e], tt[0][e], tt[1][e], tt[2][e]);
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t u0 = __float_as_uint(p[8 * c2 + e]) & 0xffff0000u;
+        const float r1 = p[8 * c2 + e] - __uint_as_float(u0);
+        const uint32_t u1 = __float_as_uint(r1) & 0xffff0000u;
+        tt[0][e] = u0;
+        tt[1][e] = u1;
+        tt[2][e] = __float_as_uint(r1 - __uint_as_float(u1));
+      }
       bf16x8 bp[3];
 #pragma unroll
       for (int t = 0; t < 3; ++t)
-        bp[t] = as_bf16x8(make_uint4(tt[t][0] | ((uint32_t)tt[t][1] << 16),
-                                     tt[t][2] | ((uint32_t)tt[t][3] << 16),
-                                     tt[t][4] | ((uint32_t)tt[t][5] << 16),
-                                     tt[t][6] | ((uint32_t)tt[t][7] << 16)));
+        bp[t] = as_bf16x8(make_uint4((tt[t][0] >> 16) | (tt[t][1] & 0xffff0000u),
+                                     (tt[t][2] >> 16) | (tt[t][3] & 0xffff0000u),
+                                     (tt[t][4] >> 16) | (tt[t][5] & 0xffff0000u),
+                                     (tt[t][6] >> 16) | (tt[t][7] & 0xffff0000u)));
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
         // V^T fragment: dimension hb 32 + rl at this lane's eight keys
