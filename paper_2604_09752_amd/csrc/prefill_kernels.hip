@@ -785,19 +785,23 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
 }
 
 // Launch over `units` (of 128 weight rows) x (R / 64) prompt-row tiles,
-// in tiles of WN / 2 units.  A product with fewer tiles than two per CU
-// also splits K over workgroups (up to kPfMaxKs slices of at least 8
-// stages), within the fix-up buffer's room: a workgroup streams its stages
-// one latency apart, so at a short prompt the 1B's QKV product (32 tiles of
-// 64 stages) took 57 us unsplit.
+// in tiles of WN / 2 units.  A product also splits K over workgroups (up
+// to kPfMaxKs slices of at least 8 stages, within the fix-up buffer's
+// room) as far as the workgroups still fit one round of the CUs: a
+// workgroup streams its stages one latency apart, so at a short prompt the
+// 1B's QKV product (32 tiles of 64 stages) took 57 us unsplit, and a split
+// past one round (the 1B's gate/up at 128 rows: 704 workgroups) leaves a
+// second, partial round.
 template <int WFMT, int EPI, int WN>
 hipError_t launch_pgemm_t(const aio_model& m, const PGemmArgs& g0, int units) {
   using Tl = PTile<WN>;
   PGemmArgs g = g0;
   const int tiles = (units + Tl::UPT - 1) / Tl::UPT;
   const int rt = (g.R + kBR - 1) / kBR, nst = g.K / kKT;
+  // workgroups one round of the CUs holds: two of 4 waves, one of 8
+  const int slots = (WN == 2 ? 2 : 1) * m.num_cus;
   g.ks = 1;
-  while (tiles * rt * g.ks < 2 * m.num_cus && 2 * g.ks <= kPfMaxKs &&
+  while (tiles * rt * 2 * g.ks <= slots && 2 * g.ks <= kPfMaxKs &&
          nst / (2 * g.ks) >= 8 &&
          (size_t)tiles * rt * 2 * g.ks * Tl::GT * 32 * 4 <= m.lay.pfix_bytes &&
          (size_t)tiles * rt <= m.lay.pcnt_n)
