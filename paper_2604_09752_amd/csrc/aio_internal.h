@@ -35,7 +35,7 @@ struct WsLayout {
   size_t vcnt;     // int32 [d/64]            arrived K slices per column tile, zeroed at load
   size_t skpart;   // fp32 [sk_tiles][kVerifySkMaxC][AIO_MAX_VERIFY_ROWS*64] stream-K shared tile sums
   size_t skcnt;    // int32 [sk_tiles]        arrived workgroups per shared tile pair, zeroed at load
-  size_t sk_tiles; // tile pairs of the largest stream-K product (QKV or gate/up)
+  size_t sk_tiles; // tile pairs of the stream-K gate/up product
   size_t pfix;     // fp32                    prefill K-slice partial tiles
   size_t pfix_bytes;
   size_t pcnt;     // int32 [pcnt_n]          arrived K slices per prefill tile, zeroed at load
@@ -63,8 +63,8 @@ struct WsLayout {
 // into; each slice's product goes to its own vpart slot.
 constexpr int kVerifyMaxKs = 8;
 
-// Most workgroups of a stream-K verify product (QKV, gate/up) that share
-// one tile pair; each has its slot of partial sums in skpart.
+// Most workgroups of the stream-K verify gate/up product that share one
+// tile pair; each has its slot of partial sums in skpart.
 constexpr int kVerifySkMaxC = 8;
 
 WsLayout aio_ws_layout(const aio_config& c);

@@ -102,11 +102,7 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.vpart = off; off = align256(off + (size_t)kVerifyMaxKs * MV * d * 4);
   L.vss = off; off = align256(off + MV * (d / 64) * 4);
   L.vcnt = off; off = align256(off + (d / 64) * 4);
-  {
-    const size_t qkv = ((size_t)c.n_heads + 2 * (size_t)c.n_kv_heads) * c.head_dim / 64;
-    const size_t gu = (F + 31) / 32;
-    L.sk_tiles = qkv > gu ? qkv : gu;
-  }
+  L.sk_tiles = (F + 31) / 32;
   L.skpart = off;
   off = align256(off + L.sk_tiles * kVerifySkMaxC * AIO_MAX_VERIFY_ROWS * 64 * 4);
   L.skcnt = off; off = align256(off + L.sk_tiles * 4);

@@ -162,7 +162,7 @@ struct VGemmArgs {
   const uint16_t* g_next;
   uint16_t* act_next;
   float* ss_out;
-  // stream-K form (QKV, SWIGLU): tile pairs of the product, and the
+  // stream-K form (SWIGLU): tile pairs of the product, and the
   // partial sums [tiles][kSkMaxC][kMaxRows * 64] and arrival counters
   // [tiles] of tile pairs that several workgroups share
   int tiles;
@@ -614,7 +614,7 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
   }
 }
 
-// Stream-K form of the QKV and gate/up products.  The product's units, a
+// Stream-K form of the gate/up product.  The product's units, a
 // tile pair (64 weight rows) times a stage of 256 k, are dealt out in equal
 // contiguous ranges in (tile pair, stage) order, one range per workgroup and
 // one workgroup per CU: every CU streams the same number of bytes, and its
@@ -627,11 +627,14 @@ __global__ __launch_bounds__(kGBlock) void k_vgemm(VGemmArgs a) {
 // the range is done, then writes them through to skpart at its slot (its
 // rank among the pair's workgroups) and counts itself in skcnt; the last to
 // arrive adds the slots in slot order, so the result does not depend on the
-// arrival order, and runs the epilogue.
+// arrival order, and runs the epilogue.  (The QKV product keeps one tile
+// pair per workgroup: its 192 pairs on 256 CUs are all shared in this form,
+// and the end-of-range hand-over made it slower.)
 constexpr int kSkMaxC = kVerifySkMaxC;  // most workgroups sharing one tile pair
 
 template <int WFMT, int EPI>
 __global__ __launch_bounds__(kGBlock, 1) void k_vgemm_sk(VGemmArgs a) {
+  static_assert(EPI == EPI_SWIGLU, "the stream-K form serves the gate/up product");
   constexpr int T = 2;
   using St = VStage<WFMT>;
   extern __shared__ __align__(16) char smem[];
@@ -676,24 +679,12 @@ __global__ __launch_bounds__(kGBlock, 1) void k_vgemm_sk(VGemmArgs a) {
     lds_off[j] = lrow[j] * St::RS + lchunk[j] * 16;
   }
   const int kend = nkb * 32 * (int)wbytes - 16;  // last 16-byte chunk of a row
-  const int qrows = a.H * a.hd, krows = a.Hkv * a.hd;
-  // first byte of weight row rr (0..63) of tile pair tp
+  // first byte of weight row rr (0..63) of tile pair tp: rows tp 32 ..
+  // tp 32 + 31 of gate (rr < 32), then the same rows of up
   auto row_ptr = [&](int tp, int rr) -> const char* {
-    const void* w;
-    int n;
-    if constexpr (EPI == EPI_QKV) {
-      const int per_head = a.hd / 64;
-      const int head = tp / per_head, sub = tp % per_head;
-      int n0 = head * a.hd + sub * 32;
-      w = a.w0;
-      if (n0 >= qrows + krows) { w = a.w2; n0 -= qrows + krows; }
-      else if (n0 >= qrows) { w = a.w1; n0 -= qrows; }
-      n = n0 + (rr >= 32 ? a.hd / 2 : 0) + (rr & 31);
-    } else {
-      w = rr >= 32 ? a.w1 : a.w0;
-      n = tp * 32 + (rr & 31);
-      if (n >= a.N) n = a.N - 1;
-    }
+    const void* w = rr >= 32 ? a.w1 : a.w0;
+    int n = tp * 32 + (rr & 31);
+    if (n >= a.N) n = a.N - 1;
     return (const char*)w + (size_t)n * a.K * wbytes;
   };
   // loads past the range re-read its last unit (and are not multiplied)
@@ -1314,7 +1305,7 @@ hipError_t launch_vgemm(const aio_model& m, const VGemmArgs& g, int blocks) {
   return hipGetLastError();
 }
 
-// Stream-K launch of a QKV or gate/up product of `tiles` tile pairs: one
+// Stream-K launch of the gate/up product of `tiles` tile pairs: one
 // workgroup per CU, but every range at least `per` units long, so that at
 // most kSkMaxC - 1 ranges meet in one tile pair (a pair of nst units spans
 // at most 1 + ceil((nst - 1) / per) ranges).
