@@ -3,11 +3,16 @@
 // single forward over its templated request: every row's K and V go to the
 // cache, and the last row's logits come out.
 //
-// Per layer: pnorm (RMSNorm + split) -> QKV GEMM (+RoPE, K/V append) ->
-// pattn (causal flash attention; row r sees positions [0, pos0 + r]; its
-// output split) -> O GEMM (+residual) -> pnorm -> gate/up GEMM (+SwiGLU,
-// split) -> down GEMM (+residual).  The last row then goes through the final
-// RMSNorm and the LM head of the verify path.
+// Per layer: QKV GEMM (+norm scale, RoPE, K/V append) -> pattn (causal
+// flash attention; row r sees positions [0, pos0 + r]; its output split) ->
+// O GEMM (+residual, split of x g for the next norm) -> gate/up GEMM (+norm
+// scale, SwiGLU, split) -> down GEMM (+residual, split of x g).  The
+// RMSNorm is folded into the products: its factor 1 / sqrt(mean(x^2) + eps)
+// is one number per row, so a residual product writes the split of x g
+// (not yet normalised) and the sums of squares of x over 64-column blocks,
+// and the consuming product scales its outputs by the row's factor.  Only
+// layer 0's embedding rows go through pnorm.  The last row then goes
+// through the final RMSNorm and the LM head of the verify path.
 //
 // Precision.  Activations stay fp32 between kernels.  The GEMMs run on MFMA
 // (v_mfma_f32_32x32x16_bf16) with every activation split exactly into three
@@ -48,6 +53,20 @@ AIO_DEV void split3(float a, uint16_t& t0, uint16_t& t1, uint16_t& t2) {
 // The split of `a` into the term planes p[0], p[ts], p[2 ts].
 AIO_DEV void store_terms(uint16_t* p, size_t ts, float a) { split3(a, p[0], p[ts], p[2 * ts]); }
 
+// The split of four consecutive values, one 8-byte store per term plane
+// (p 8-byte aligned).
+AIO_DEV void store_terms4(uint16_t* p, size_t ts, float4 a) {
+  uint16_t t[4][kNT];
+  split3(a.x, t[0][0], t[0][1], t[0][2]);
+  split3(a.y, t[1][0], t[1][1], t[1][2]);
+  split3(a.z, t[2][0], t[2][1], t[2][2]);
+  split3(a.w, t[3][0], t[3][1], t[3][2]);
+#pragma unroll
+  for (int k = 0; k < kNT; ++k)
+    *(uint2*)(p + k * ts) = make_uint2((uint32_t)t[0][k] | ((uint32_t)t[1][k] << 16),
+                                       (uint32_t)t[2][k] | ((uint32_t)t[3][k] << 16));
+}
+
 // Device-coherent access for the K slices of a split product: the partials
 // are written through to memory and read past the (per-XCD) L2, and the
 // slice counters are vector atomics at device scope.
@@ -77,43 +96,37 @@ struct PNormArgs {
   const uint16_t* embed;   // layer 0: embedding table, else null
   const int32_t* tokens;   // [R] (layer 0)
   const uint16_t* gain;
-  uint16_t* act;           // [kNT][R][lda]: terms of the normalised rows
+  uint16_t* act;           // [kNT][R][lda]: terms of x g
   int lda;
   size_t tstride;          // elements between term planes
   int d;
-  float eps;
+  float* ss;               // [R][d / 64] sums of squares of x over 64-column blocks
 };
 
 constexpr int kNormThreads = 256;
 
-// One workgroup per row: h = x / sqrt(mean(x^2) + eps) * g, split.
+// One workgroup per row (layer 0): x from the embedding table, the split of
+// x g, and the row's sums of squares of x per 64-column block.
 __global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
-  __shared__ float red[kNormThreads / AIO_WAVE];
   const int r = blockIdx.x, tid = threadIdx.x;
   float* xr = a.x + (size_t)r * a.d;
   const uint16_t* emb = a.embed ? a.embed + (size_t)a.tokens[r] * a.d : nullptr;
-  float ss = 0.f;
-  for (int e = tid; e < a.d; e += kNormThreads) {
-    float v;
-    if (emb) {
-      v = bf16_to_f32(emb[e]);
-      xr[e] = v;
-    } else {
-      v = xr[e];
-    }
-    ss = fmaf(v, v, ss);
-  }
-  ss = wave_sum(ss);
-  if ((tid & (AIO_WAVE - 1)) == 0) red[tid / AIO_WAVE] = ss;
-  __syncthreads();
-  float tot = 0.f;
-#pragma unroll
-  for (int w = 0; w < kNormThreads / AIO_WAVE; ++w) tot += red[w];
-  const float inv = rsqrtf(tot / (float)a.d + a.eps);
   uint16_t* out = a.act + (size_t)r * a.lda;
-  for (int e = tid; e < a.d; e += kNormThreads) {
-    const float v = (emb ? bf16_to_f32(emb[e]) : xr[e]) * inv * bf16_to_f32(a.gain[e]);
-    store_terms(out + e, a.tstride, v);
+  // a wave covers one 64-column block per pass (d is a multiple of 64)
+  for (int e0 = 0; e0 < a.d; e0 += kNormThreads) {
+    const int e = e0 + tid;
+    float v = 0.f;
+    if (e < a.d) {
+      if (emb) {
+        v = bf16_to_f32(emb[e]);
+        xr[e] = v;
+      } else {
+        v = xr[e];
+      }
+      store_terms(out + e, a.tstride, v * bf16_to_f32(a.gain[e]));
+    }
+    const float sq = wave_sum(v * v);
+    if ((tid & (AIO_WAVE - 1)) == 0 && e < a.d) a.ss[(size_t)r * (a.d / 64) + e / 64] = sq;
   }
 }
 
@@ -182,6 +195,17 @@ struct PGemmArgs {
   int ks;
   float* fix;           // [tiles][ks][32][threads]
   int* tcnt;            // [tiles], zero between products
+  // the folded RMSNorm: QKV and SWIGLU scale output row r by 1 / sqrt(sum
+  // of ss_in[r][0 .. nss) / K + eps); RESID (with act_next) writes the split
+  // of x g_next to act_next and ss_out[r][n / 64] for its columns
+  const float* ss_in;
+  float* ss_out;
+  int nss;
+  float eps;
+  uint16_t* act_next;
+  int lda_next;
+  size_t tstride_next;
+  const uint16_t* g_next;
 };
 
 // Where block `blk` (0..3) of unit `bx` reads its 32 rows: matrix index
@@ -373,6 +397,28 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
   const int sL = sB - 1;
   gload_stage<WFMT, WN, A_LD>(aptr, bptr, sA, ra_, rb_);
   gload_stage<WFMT, WN, A_LD>(aptr, bptr, min(sA + 1, sL), ra1, rb1);
+  // the folded norm's row factors of the tile's 64 prompt rows, Tl::GT / 64
+  // threads per row (their loads queue behind the first stages'; the
+  // barrier below publishes them)
+  __shared__ float inv_rows[kBR];
+  if constexpr (EPI != PE_RESID) {
+    constexpr int TPR = Tl::GT / kBR;
+    const int j = tid / TPR, part = tid % TPR;
+    const float* ssr = a.ss_in + (size_t)min(r0 + j, a.R - 1) * a.nss;
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    int c = part;
+    for (; c + 3 * TPR < a.nss; c += 4 * TPR) {
+      s0 += ssr[c];
+      s1 += ssr[c + TPR];
+      s2 += ssr[c + 2 * TPR];
+      s3 += ssr[c + 3 * TPR];
+    }
+    for (; c < a.nss; c += TPR) s0 += ssr[c];
+    float sum = (s0 + s1) + (s2 + s3);
+#pragma unroll
+    for (int off = TPR / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, AIO_WAVE);
+    if (part == 0) inv_rows[j] = rsqrtf(sum / (float)a.K + a.eps);
+  }
   lstore_stage<WFMT, WN, A_LD>(smem, alds, blds, ra_, rb_);
   __syncthreads();
   gload_stage<WFMT, WN, A_LD>(aptr, bptr, min(sA + 2, sL), ra_, rb_);
@@ -455,10 +501,80 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
   if (r >= a.R) return;
   const BlockSrc slo = block_src<EPI>(a, Tl::UPT * bx + (wn >> 1), 2 * (wn & 1));
   const BlockSrc shi = block_src<EPI>(a, Tl::UPT * bx + (wn >> 1), 2 * (wn & 1) + 1);
+  if constexpr (EPI == PE_RESID) {
+    // N is a multiple of 64: the wave's two blocks (adjacent, from a
+    // multiple of 64) are both whole or both past the end.  The lane's 16
+    // values of a block are 4 runs of 4 columns: x moves as float4, the
+    // split of x g as one 8-byte store per term.
+    if (!slo.valid) return;
+    float* xrow = a.out + (size_t)r * a.ldo;
+    float sq = 0.f;  // the lane's sum of squares of the new x
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      const int nb = (hb ? shi.row0 : slo.row0) + 4 * kh;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = nb + 8 * g;
+        float y[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          y[e] = hb ? yhi[4 * g + e] : ylo[4 * g + e];
+          if constexpr (WFMT == AIO_WFMT_INT8) y[e] *= fp16_to_f32(a.s0[n + e]);
+        }
+        float4* xp = (float4*)(xrow + n);
+        float4 xn = *xp;
+        xn.x += y[0];
+        xn.y += y[1];
+        xn.z += y[2];
+        xn.w += y[3];
+        *xp = xn;
+        if (a.act_next) {
+          const uint16_t* gn = a.g_next + n;
+          store_terms4(a.act_next + (size_t)r * a.lda_next + n, a.tstride_next,
+                       make_float4(xn.x * bf16_to_f32(gn[0]), xn.y * bf16_to_f32(gn[1]),
+                                   xn.z * bf16_to_f32(gn[2]), xn.w * bf16_to_f32(gn[3])));
+          sq = fmaf(xn.x, xn.x, sq);
+          sq = fmaf(xn.y, xn.y, sq);
+          sq = fmaf(xn.z, xn.z, sq);
+          sq = fmaf(xn.w, xn.w, sq);
+        }
+      }
+    }
+    // the wave's 64 columns are one block of the sums for row r: this lane
+    // holds 32 of them, the lane 32 away (same row) the other 32
+    if (a.act_next) {
+      sq += __shfl_xor(sq, 32, AIO_WAVE);
+      if (kh == 0) a.ss_out[(size_t)r * a.nss + slo.row0 / 64] = sq;
+    }
+    return;
+  }
+  const float rs = inv_rows[wr * 32 + rl];
+  if constexpr (EPI == PE_SWIGLU) {
+    // F is a multiple of 64: the block is whole or past the end; the lane's
+    // 16 values are 4 runs of 4 columns, one 8-byte store per term each
+    if (!slo.valid) return;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = slo.row0 + 8 * g + 4 * kh;
+      float h[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float gt = ylo[4 * g + e] * rs, up = yhi[4 * g + e] * rs;
+        if constexpr (WFMT == AIO_WFMT_INT8) {
+          gt *= fp16_to_f32(a.s0[n + e]);
+          up *= fp16_to_f32(a.s1[n + e]);
+        }
+        h[e] = gt / (1.f + expf(-gt)) * up;
+      }
+      store_terms4(a.act_out + (size_t)r * a.lda_out + n, a.tstride_out,
+                   make_float4(h[0], h[1], h[2], h[3]));
+    }
+    return;
+  }
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int i = 8 * (v / 4) + 4 * kh + (v % 4);
-    float ylo_v = ylo[v], yhi_v = yhi[v];
+    float ylo_v = ylo[v] * rs, yhi_v = yhi[v] * rs;
     if constexpr (EPI == PE_QKV) {
       if (slo.valid == 0) continue;
       const int half = a.hd / 2;
@@ -486,26 +602,6 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
         uint16_t* c = (mat == 1 ? a.kc : a.vc) + ((size_t)g * a.max_ctx + p) * a.hd;
         c[ii] = f32_to_bf16(ylo_v);
         c[ii + half] = f32_to_bf16(yhi_v);
-      }
-    } else if constexpr (EPI == PE_SWIGLU) {
-      if (i >= slo.valid) continue;
-      const int n = slo.row0 + i;
-      if constexpr (WFMT == AIO_WFMT_INT8) {
-        ylo_v *= fp16_to_f32(a.s0[n]);
-        yhi_v *= fp16_to_f32(a.s1[n]);
-      }
-      store_terms(a.act_out + (size_t)r * a.lda_out + n, a.tstride_out,
-                  ylo_v / (1.f + expf(-ylo_v)) * yhi_v);
-    } else {
-      if (i < slo.valid) {
-        const int n = slo.row0 + i;
-        if constexpr (WFMT == AIO_WFMT_INT8) ylo_v *= fp16_to_f32(a.s0[n]);
-        a.out[(size_t)r * a.ldo + n] += ylo_v;
-      }
-      if (i < shi.valid) {
-        const int n = shi.row0 + i;
-        if constexpr (WFMT == AIO_WFMT_INT8) yhi_v *= fp16_to_f32(a.s0[n]);
-        a.out[(size_t)r * a.ldo + n] += yhi_v;
       }
     }
   }
@@ -779,7 +875,7 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
   n.lda = b.lda_a;
   n.tstride = (size_t)b.rcap * b.lda_a;
   n.d = m.cfg.d_model;
-  n.eps = m.cfg.rms_eps;
+  n.ss = b.ss;
   hipLaunchKernelGGL(k_pnorm, dim3(R), dim3(kNormThreads), 0, m.stream, n);
   return hipGetLastError();
 }
@@ -847,7 +943,7 @@ hipError_t launch_pattn_t(const aio_model& m, const PAttnArgs& t) {
 size_t aio_prefill_row_bytes(const aio_config& c) {
   const size_t d = (size_t)c.d_model, Hd = (size_t)c.n_heads * c.head_dim, F = (size_t)c.ffn_dim;
   const size_t ka = d > Hd ? d : Hd;
-  return 4 + 4 * d + 4 * Hd + 2 * kNT * ka + 2 * kNT * F;
+  return 4 + 4 * d + 4 * Hd + 2 * kNT * ka + 2 * kNT * d + 2 * kNT * F + 4 * (d / 64);
 }
 
 PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
@@ -862,7 +958,9 @@ PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
   b.x = (float*)(base + off); off = al(off + 4 * d * rcap);
   b.q = (float*)(base + off); off = al(off + 4 * Hd * rcap);
   b.actA = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_a * rcap);
+  b.actN = (uint16_t*)(base + off); off = al(off + 2 * kNT * d * rcap);
   b.actB = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_b * rcap);
+  b.ss = (float*)(base + off); off = al(off + 4 * (d / 64) * rcap);
   b.bytes = off;
   return b;
 }
@@ -874,15 +972,21 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
   const aio_config& c = m.cfg;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const size_t tsA = (size_t)b.rcap * b.lda_a, tsB = (size_t)b.rcap * b.lda_b;
+  const size_t tsN = (size_t)b.rcap * d;
+  const int nss = d / 64;
   hipError_t e;
+  // layer 0's input rows: the embeddings, with the split of x g and the
+  // sums of squares for its attention norm; every later norm input comes
+  // from the residual product before it
+  if ((e = launch_pnorm(m, b, R, (const uint16_t*)m.embed, m.layers[0].attn_norm)) != hipSuccess)
+    return e;
   for (int l = 0; l < c.n_layers; ++l) {
     const aio_layer_weights& L = m.layers[(size_t)l];
-    if ((e = launch_pnorm(m, b, R, l == 0 ? (const uint16_t*)m.embed : nullptr, L.attn_norm)) !=
-        hipSuccess)
-      return e;
+    const bool last = l + 1 == c.n_layers;
 
     PGemmArgs g{};
     g.act = b.actA; g.lda = b.lda_a; g.tstride = tsA; g.R = R;
+    g.ss_in = b.ss; g.nss = nss; g.eps = c.rms_eps;
     g.w0 = L.wq; g.w1 = L.wk; g.w2 = L.wv;
     g.s0 = (const uint16_t*)L.sq; g.s1 = (const uint16_t*)L.sk; g.s2 = (const uint16_t*)L.sv;
     g.N = (H + 2 * Hkv) * hd; g.K = d;
@@ -906,11 +1010,13 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     o.act = b.actA; o.lda = b.lda_a; o.tstride = tsA; o.R = R;
     o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
     o.N = d; o.K = H * hd; o.out = b.x; o.ldo = d;
+    o.act_next = b.actN; o.lda_next = d; o.tstride_next = tsN;
+    o.g_next = (const uint16_t*)L.ffn_norm; o.ss_out = b.ss; o.nss = nss;
     if ((e = launch_pgemm<PE_RESID>(m, o, (d + kUnit - 1) / kUnit)) != hipSuccess) return e;
 
-    if ((e = launch_pnorm(m, b, R, nullptr, L.ffn_norm)) != hipSuccess) return e;
     PGemmArgs gu{};
-    gu.act = b.actA; gu.lda = b.lda_a; gu.tstride = tsA; gu.R = R;
+    gu.act = b.actN; gu.lda = d; gu.tstride = tsN; gu.R = R;
+    gu.ss_in = b.ss; gu.nss = nss; gu.eps = c.rms_eps;
     gu.w0 = L.w_gate; gu.w1 = L.w_up;
     gu.s0 = (const uint16_t*)L.s_gate; gu.s1 = (const uint16_t*)L.s_up;
     gu.N = F; gu.K = d;
@@ -921,6 +1027,11 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     dn.act = b.actB; dn.lda = b.lda_b; dn.tstride = tsB; dn.R = R;
     dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
     dn.N = d; dn.K = F; dn.out = b.x; dn.ldo = d;
+    if (!last) {
+      dn.act_next = b.actA; dn.lda_next = b.lda_a; dn.tstride_next = tsA;
+      dn.g_next = (const uint16_t*)m.layers[(size_t)l + 1].attn_norm;
+      dn.ss_out = b.ss; dn.nss = nss;
+    }
     if ((e = launch_pgemm<PE_RESID>(m, dn, (d + kUnit - 1) / kUnit)) != hipSuccess) return e;
   }
   return hipSuccess;
