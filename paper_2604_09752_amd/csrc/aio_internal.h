@@ -147,9 +147,9 @@ struct PfBuffers {
   int32_t* tokens;  // [rcap]
   float* x;         // [rcap][d] residual rows
   float* q;         // [rcap][H hd] rotated queries
-  uint16_t* actA;   // [3][rcap][lda_a] split activations: QKV input (x g), O input
-  uint16_t* actN;   // [3][rcap][d] split x g of the pre-FFN norm: the gate/up input
-  uint16_t* actB;   // [3][rcap][lda_b] split SwiGLU output: the down input
+  float* actA;      // [rcap][lda_a] activations: QKV input (x g), O input
+  float* actN;      // [rcap][d] x g of the pre-FFN norm: the gate/up input
+  float* actB;      // [rcap][lda_b] SwiGLU output: the down input
   float* ss;        // [rcap][d / 64] sums of squares of x over 64-column blocks
   int rcap, lda_a, lda_b;
   size_t bytes;     // total, every region 256-byte aligned

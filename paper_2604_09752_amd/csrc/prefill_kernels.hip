@@ -4,19 +4,19 @@
 // cache, and the last row's logits come out.
 //
 // Per layer: QKV GEMM (+norm scale, RoPE, K/V append) -> pattn (causal
-// flash attention; row r sees positions [0, pos0 + r]; its output split) ->
-// O GEMM (+residual, split of x g for the next norm) -> gate/up GEMM (+norm
-// scale, SwiGLU, split) -> down GEMM (+residual, split of x g).  The
-// RMSNorm is folded into the products: its factor 1 / sqrt(mean(x^2) + eps)
-// is one number per row, so a residual product writes the split of x g
-// (not yet normalised) and the sums of squares of x over 64-column blocks,
-// and the consuming product scales its outputs by the row's factor.  Only
-// layer 0's embedding rows go through pnorm.  The last row then goes
-// through the final RMSNorm and the LM head of the verify path.
+// flash attention; row r sees positions [0, pos0 + r]) -> O GEMM
+// (+residual, x g for the next norm) -> gate/up GEMM (+norm scale, SwiGLU)
+// -> down GEMM (+residual, x g).  The RMSNorm is folded into the products:
+// its factor 1 / sqrt(mean(x^2) + eps) is one number per row, so a residual
+// product writes x g (not yet normalised) and the sums of squares of x over
+// 64-column blocks, and the consuming product scales its outputs by the
+// row's factor.  Only layer 0's embedding rows go through pnorm.  The last
+// row then goes through the final RMSNorm and the LM head of the verify
+// path.
 //
 // Precision.  Activations stay fp32 between kernels.  The GEMMs run on MFMA
 // (v_mfma_f32_32x32x16_bf16) with every activation split exactly into three
-// bf16 terms, a = t0 + t1 + t2 + r with |r| <= 2^-27 |a|, so the products
+// bf16 terms as it is staged in LDS, a = t0 + t1 + t2 + r with |r| <= 2^-27 |a|, so the products
 // keep fp32 accuracy (two terms leave 2^-18, which measurably loosens the
 // cache rows of deeper layers).  Weights are exact in bf16 (int8 weights
 // convert exactly; their fp16 per-output-channel scale applies in the
@@ -31,6 +31,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 AIO_DEV f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -41,30 +42,18 @@ AIO_DEV bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 // Terms of the activation split.
 constexpr int kNT = 3;
 
-// Exact three-term bf16 split: t0 = bf16(a), t1 = bf16(a - t0),
-// t2 = bf16(a - t0 - t1) (each subtraction is exact in fp32).
-AIO_DEV void split3(float a, uint16_t& t0, uint16_t& t1, uint16_t& t2) {
-  t0 = f32_to_bf16(a);
-  const float r1 = a - bf16_to_f32(t0);
-  t1 = f32_to_bf16(r1);
-  t2 = f32_to_bf16(r1 - bf16_to_f32(t1));
-}
-
-// The split of `a` into the term planes p[0], p[ts], p[2 ts].
-AIO_DEV void store_terms(uint16_t* p, size_t ts, float a) { split3(a, p[0], p[ts], p[2 * ts]); }
-
-// The split of four consecutive values, one 8-byte store per term plane
-// (p 8-byte aligned).
-AIO_DEV void store_terms4(uint16_t* p, size_t ts, float4 a) {
-  uint16_t t[4][kNT];
-  split3(a.x, t[0][0], t[0][1], t[0][2]);
-  split3(a.y, t[1][0], t[1][1], t[1][2]);
-  split3(a.z, t[2][0], t[2][1], t[2][2]);
-  split3(a.w, t[3][0], t[3][1], t[3][2]);
-#pragma unroll
-  for (int k = 0; k < kNT; ++k)
-    *(uint2*)(p + k * ts) = make_uint2((uint32_t)t[0][k] | ((uint32_t)t[1][k] << 16),
-                                       (uint32_t)t[2][k] | ((uint32_t)t[3][k] << 16));
+// Three-term bf16 split by truncation, for fp32 bits `a`: t0 = the top 16
+// bits of a, t1 those of r1 = a - t0, t2 those of r1 - t1.  Both
+// subtractions are exact and r1 - t1 has at most 8 significant bits, so a =
+// t0 + t1 + t2 exactly (for a normal, as every activation here is).
+// Returned as fp32 bit patterns with the low 16 bits clear (the bf16 in the
+// high half); branch-free.  (Rounding to nearest instead costs several
+// times the operations, and in the stage loader its registers spilled.)
+AIO_DEV void split3t(uint32_t a, uint32_t (&t)[kNT]) {
+  t[0] = a & 0xffff0000u;
+  const float r1 = __uint_as_float(a) - __uint_as_float(t[0]);
+  t[1] = __float_as_uint(r1) & 0xffff0000u;
+  t[2] = __float_as_uint(r1 - __uint_as_float(t[1])) & 0xffff0000u;
 }
 
 // Device-coherent access for the K slices of a split product: the partials
@@ -96,22 +85,21 @@ struct PNormArgs {
   const uint16_t* embed;   // layer 0: embedding table, else null
   const int32_t* tokens;   // [R] (layer 0)
   const uint16_t* gain;
-  uint16_t* act;           // [kNT][R][lda]: terms of x g
+  float* act;              // [R][lda]: x g
   int lda;
-  size_t tstride;          // elements between term planes
   int d;
   float* ss;               // [R][d / 64] sums of squares of x over 64-column blocks
 };
 
 constexpr int kNormThreads = 256;
 
-// One workgroup per row (layer 0): x from the embedding table, the split of
-// x g, and the row's sums of squares of x per 64-column block.
+// One workgroup per row (layer 0): x from the embedding table, x g, and the
+// row's sums of squares of x per 64-column block.
 __global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
   const int r = blockIdx.x, tid = threadIdx.x;
   float* xr = a.x + (size_t)r * a.d;
   const uint16_t* emb = a.embed ? a.embed + (size_t)a.tokens[r] * a.d : nullptr;
-  uint16_t* out = a.act + (size_t)r * a.lda;
+  float* out = a.act + (size_t)r * a.lda;
   // a wave covers one 64-column block per pass (d is a multiple of 64)
   for (int e0 = 0; e0 < a.d; e0 += kNormThreads) {
     const int e = e0 + tid;
@@ -123,7 +111,7 @@ __global__ __launch_bounds__(kNormThreads) void k_pnorm(PNormArgs a) {
       } else {
         v = xr[e];
       }
-      store_terms(out + e, a.tstride, v * bf16_to_f32(a.gain[e]));
+      out[e] = v * bf16_to_f32(a.gain[e]);
     }
     const float sq = wave_sum(v * v);
     if ((tid & (AIO_WAVE - 1)) == 0 && e < a.d) a.ss[(size_t)r * (a.d / 64) + e / 64] = sq;
@@ -152,7 +140,7 @@ constexpr int kBR = 64;   // prompt rows per tile
 constexpr int kKT = 32;   // k per stage
 constexpr int kRowB = kKT * 2 + 16;
 constexpr int kBCols = kNT * kBR;                  // activation columns: term-major per wave half
-constexpr int kBChunks = kBCols * (kKT / 8);       // 16-byte activation chunks per stage
+constexpr int kBChunks = kBR * (kKT / 4);         // 16-byte (4 x fp32) activation chunks per stage
 
 // The tile shape of WN waves across the weight rows.
 template <int WN>
@@ -168,9 +156,8 @@ struct PTile {
 enum PEpi { PE_QKV = 0, PE_RESID = 1, PE_SWIGLU = 2 };
 
 struct PGemmArgs {
-  const uint16_t* act;  // [kNT][R][lda] split activations
+  const float* act;     // [R][lda] activations (split into terms on the way to LDS)
   int lda;
-  size_t tstride;
   int R;
   const void* w0;       // QKV: wq | SWIGLU: w_gate | RESID: the matrix
   const void* w1;       // QKV: wk | SWIGLU: w_up
@@ -181,9 +168,8 @@ struct PGemmArgs {
   int N, K;             // QKV: N = (H + 2 Hkv) hd virtual rows; SWIGLU: F; RESID: rows
   float* out;           // QKV: q [R][H hd] | RESID: x [R][N]
   int ldo;
-  uint16_t* act_out;    // SWIGLU: [kNT][R][lda_out]
+  float* act_out;       // SWIGLU: [R][lda_out]
   int lda_out;
-  size_t tstride_out;
   uint16_t* kc;         // QKV: cache of the layer, [Hkv][max_ctx][hd]
   uint16_t* vc;
   const float2* rope;   // [max_ctx][hd / 2] (cos, sin)
@@ -196,15 +182,14 @@ struct PGemmArgs {
   float* fix;           // [tiles][ks][32][threads]
   int* tcnt;            // [tiles], zero between products
   // the folded RMSNorm: QKV and SWIGLU scale output row r by 1 / sqrt(sum
-  // of ss_in[r][0 .. nss) / K + eps); RESID (with act_next) writes the split
-  // of x g_next to act_next and ss_out[r][n / 64] for its columns
+  // of ss_in[r][0 .. nss) / K + eps); RESID (with act_next) writes x g_next
+  // to act_next and ss_out[r][n / 64] for its columns
   const float* ss_in;
   float* ss_out;
   int nss;
   float eps;
-  uint16_t* act_next;
+  float* act_next;
   int lda_next;
-  size_t tstride_next;
   const uint16_t* g_next;
 };
 
@@ -262,7 +247,7 @@ AIO_DEV const char* pick_mat(const PGemmArgs& a, int mat) {
 // Global loads of stage st: A_LD 16-byte weight chunks and BLD activation
 // chunks per thread.
 template <int WFMT, int WN, int A_LD, int BLD = PTile<WN>::BLd>
-AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const (&bptr)[BLD],
+AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const float* const (&bptr)[BLD],
                          int st, uint4 (&ra)[A_LD], uint4 (&rb)[BLD]) {
   constexpr int GT = PTile<WN>::GT;
   constexpr int wbytes = WFMT == AIO_WFMT_BF16 ? 2 : 1;
@@ -275,8 +260,9 @@ AIO_DEV void gload_stage(const char* const (&aptr)[A_LD], const uint16_t* const 
       rb[j] = *(const uint4*)(bptr[j] + ko);
 }
 
-// The same chunks into an LDS stage buffer (int8 widened to bf16, exact:
-// |q| <= 127).
+// The same chunks into an LDS stage buffer: int8 widened to bf16 (exact:
+// |q| <= 127); each activation value split into its three bf16 terms, one
+// 8-byte store per term column (4 consecutive k).
 template <int WFMT, int WN, int A_LD, int BLD = PTile<WN>::BLd>
 AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[BLD],
                           const uint4 (&ra)[A_LD], const uint4 (&rb)[BLD]) {
@@ -306,8 +292,16 @@ AIO_DEV void lstore_stage(char* buf, const int (&alds)[A_LD], const int (&blds)[
 #pragma unroll
   for (int j = 0; j < BLD; ++j)
     if (j + 1 < BLD || kBChunks % GT == 0 || (int)threadIdx.x < kBChunks % GT) {
-      const u32x4 w = {rb[j].x, rb[j].y, rb[j].z, rb[j].w};
-      *(u32x4*)(buf + blds[j]) = w;
+      uint32_t t[4][kNT];
+      split3t(rb[j].x, t[0]);
+      split3t(rb[j].y, t[1]);
+      split3t(rb[j].z, t[2]);
+      split3t(rb[j].w, t[3]);
+#pragma unroll
+      for (int k = 0; k < kNT; ++k) {
+        const u32x2 w = {(t[0][k] >> 16) | t[1][k], (t[2][k] >> 16) | t[3][k]};
+        *(u32x2*)(buf + blds[j] + k * 32 * kRowB) = w;
+      }
     }
 }
 
@@ -349,9 +343,9 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
 
   // Staging assignments.  A: row ra of the tile (block ra / 32), 16-byte
   // chunk ca of the stage's 32 k (bf16: 4 chunks of 8 weights; int8: 2
-  // chunks of 16 weights, widened to 32 bytes in LDS).  B: activation column
-  // cb = (wr' kNT + t) 32 + j -> prompt row r0 + 32 wr' + j, term t; 4
-  // chunks of 8 k.
+  // chunks of 16 weights, widened to 32 bytes in LDS).  B: prompt row r0 +
+  // p (p = 32 wr' + j), 8 chunks of 4 fp32 k; its terms t go to the LDS
+  // activation columns (wr' kNT + t) 32 + j.
   constexpr int A_CPR = WFMT == AIO_WFMT_BF16 ? 4 : 2;
   constexpr int A_LD = kBM * A_CPR / kGT;
   const char* aptr[A_LD];
@@ -367,15 +361,14 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
     aptr[j] = w + ((size_t)row * a.K + (size_t)ca * (16 / wbytes)) * wbytes;
     alds[j] = ra * kRowB + ca * 16 * (2 / wbytes);
   }
-  const uint16_t* bptr[kBLd];
+  const float* bptr[kBLd];
   int blds[kBLd];
 #pragma unroll
   for (int j = 0; j < kBLd; ++j) {
-    const int f = min(j * kGT + tid, kBChunks - 1), cb = f / 4, c = f % 4;
-    const int half = cb / (kNT * 32), t = (cb / 32) % kNT;
-    const int row = r0 + half * 32 + (cb & 31);
-    bptr[j] = a.act + t * a.tstride + (size_t)(row < a.R ? row : a.R - 1) * a.lda + c * 8;
-    blds[j] = (kBM + cb) * kRowB + c * 16;
+    const int f = min(j * kGT + tid, kBChunks - 1), p = f / 8, c = f % 8;
+    const int row = r0 + p;
+    bptr[j] = a.act + (size_t)(row < a.R ? row : a.R - 1) * a.lda + c * 4;
+    blds[j] = (kBM + (p / 32) * kNT * 32 + (p % 32)) * kRowB + c * 8;
   }
   uint4 ra_[A_LD], rb_[kBLd];
   f32x16 acc[2][kNT];
@@ -504,8 +497,7 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
   if constexpr (EPI == PE_RESID) {
     // N is a multiple of 64: the wave's two blocks (adjacent, from a
     // multiple of 64) are both whole or both past the end.  The lane's 16
-    // values of a block are 4 runs of 4 columns: x moves as float4, the
-    // split of x g as one 8-byte store per term.
+    // values of a block are 4 runs of 4 columns, moved as float4.
     if (!slo.valid) return;
     float* xrow = a.out + (size_t)r * a.ldo;
     float sq = 0.f;  // the lane's sum of squares of the new x
@@ -530,9 +522,9 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
         *xp = xn;
         if (a.act_next) {
           const uint16_t* gn = a.g_next + n;
-          store_terms4(a.act_next + (size_t)r * a.lda_next + n, a.tstride_next,
-                       make_float4(xn.x * bf16_to_f32(gn[0]), xn.y * bf16_to_f32(gn[1]),
-                                   xn.z * bf16_to_f32(gn[2]), xn.w * bf16_to_f32(gn[3])));
+          *(float4*)(a.act_next + (size_t)r * a.lda_next + n) =
+              make_float4(xn.x * bf16_to_f32(gn[0]), xn.y * bf16_to_f32(gn[1]),
+                          xn.z * bf16_to_f32(gn[2]), xn.w * bf16_to_f32(gn[3]));
           sq = fmaf(xn.x, xn.x, sq);
           sq = fmaf(xn.y, xn.y, sq);
           sq = fmaf(xn.z, xn.z, sq);
@@ -551,7 +543,7 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
   const float rs = inv_rows[wr * 32 + rl];
   if constexpr (EPI == PE_SWIGLU) {
     // F is a multiple of 64: the block is whole or past the end; the lane's
-    // 16 values are 4 runs of 4 columns, one 8-byte store per term each
+    // 16 values are 4 runs of 4 columns, one float4 store each
     if (!slo.valid) return;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
@@ -566,8 +558,7 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
         }
         h[e] = gt / (1.f + expf(-gt)) * up;
       }
-      store_terms4(a.act_out + (size_t)r * a.lda_out + n, a.tstride_out,
-                   make_float4(h[0], h[1], h[2], h[3]));
+      *(float4*)(a.act_out + (size_t)r * a.lda_out + n) = make_float4(h[0], h[1], h[2], h[3]);
     }
     return;
   }
@@ -614,9 +605,8 @@ struct PAttnArgs {
   int ldq;
   const uint16_t* kc;   // [Hkv][max_ctx][hd]
   const uint16_t* vc;
-  uint16_t* act;        // [kNT][R][lda]: the output, split, at columns h hd ..
+  float* act;           // [R][lda]: the output, at columns h hd ..
   int lda;
-  size_t tstride;
   int R, pos0, H, Hkv, max_ctx;
   float scale_log2;     // log2(e) / sqrt(hd)
 };
@@ -852,14 +842,15 @@ __global__ __launch_bounds__(kAW * AIO_WAVE, 2) void k_pattn(PAttnArgs a) {
   if (rl >= rows) return;
   const int r = q0 + rl;
   const float inv = 1.f / lsum;
-  uint16_t* out = a.act + (size_t)r * a.lda + (size_t)h * HD;
+  float* out = a.act + (size_t)r * a.lda + (size_t)h * HD;
+  // the lane's dimensions come in runs of 4: one float4 store each
 #pragma unroll
   for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int dim = hb * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-      store_terms(out + dim, a.tstride, o[hb][v] * inv);
-    }
+    for (int g = 0; g < 4; ++g)
+      *(float4*)(out + hb * 32 + 8 * g + 4 * kh) =
+          make_float4(o[hb][4 * g] * inv, o[hb][4 * g + 1] * inv, o[hb][4 * g + 2] * inv,
+                      o[hb][4 * g + 3] * inv);
 }
 
 // ----------------------------------------------------------------- launchers
@@ -873,7 +864,6 @@ hipError_t launch_pnorm(const aio_model& m, const PfBuffers& b, int R, const uin
   n.gain = (const uint16_t*)gain;
   n.act = b.actA;
   n.lda = b.lda_a;
-  n.tstride = (size_t)b.rcap * b.lda_a;
   n.d = m.cfg.d_model;
   n.ss = b.ss;
   hipLaunchKernelGGL(k_pnorm, dim3(R), dim3(kNormThreads), 0, m.stream, n);
@@ -943,7 +933,7 @@ hipError_t launch_pattn_t(const aio_model& m, const PAttnArgs& t) {
 size_t aio_prefill_row_bytes(const aio_config& c) {
   const size_t d = (size_t)c.d_model, Hd = (size_t)c.n_heads * c.head_dim, F = (size_t)c.ffn_dim;
   const size_t ka = d > Hd ? d : Hd;
-  return 4 + 4 * d + 4 * Hd + 2 * kNT * ka + 2 * kNT * d + 2 * kNT * F + 4 * (d / 64);
+  return 4 + 4 * d + 4 * Hd + 4 * ka + 4 * d + 4 * F + 4 * (d / 64);
 }
 
 PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
@@ -957,9 +947,9 @@ PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
   b.tokens = (int32_t*)(base + off); off = al(off + 4 * (size_t)rcap);
   b.x = (float*)(base + off); off = al(off + 4 * d * rcap);
   b.q = (float*)(base + off); off = al(off + 4 * Hd * rcap);
-  b.actA = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_a * rcap);
-  b.actN = (uint16_t*)(base + off); off = al(off + 2 * kNT * d * rcap);
-  b.actB = (uint16_t*)(base + off); off = al(off + 2 * kNT * (size_t)b.lda_b * rcap);
+  b.actA = (float*)(base + off); off = al(off + 4 * (size_t)b.lda_a * rcap);
+  b.actN = (float*)(base + off); off = al(off + 4 * d * rcap);
+  b.actB = (float*)(base + off); off = al(off + 4 * (size_t)b.lda_b * rcap);
   b.ss = (float*)(base + off); off = al(off + 4 * (d / 64) * rcap);
   b.bytes = off;
   return b;
@@ -971,8 +961,6 @@ PfBuffers aio_prefill_buffers(const aio_config& c, char* base, int rcap) {
 hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int R, int pos0) {
   const aio_config& c = m.cfg;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
-  const size_t tsA = (size_t)b.rcap * b.lda_a, tsB = (size_t)b.rcap * b.lda_b;
-  const size_t tsN = (size_t)b.rcap * d;
   const int nss = d / 64;
   hipError_t e;
   // layer 0's input rows: the embeddings, with the split of x g and the
@@ -985,7 +973,7 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     const bool last = l + 1 == c.n_layers;
 
     PGemmArgs g{};
-    g.act = b.actA; g.lda = b.lda_a; g.tstride = tsA; g.R = R;
+    g.act = b.actA; g.lda = b.lda_a; g.R = R;
     g.ss_in = b.ss; g.nss = nss; g.eps = c.rms_eps;
     g.w0 = L.wq; g.w1 = L.wk; g.w2 = L.wv;
     g.s0 = (const uint16_t*)L.sq; g.s1 = (const uint16_t*)L.sk; g.s2 = (const uint16_t*)L.sv;
@@ -1000,35 +988,35 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
     PAttnArgs t{};
     t.q = b.q; t.ldq = H * hd;
     t.kc = g.kc; t.vc = g.vc;
-    t.act = b.actA; t.lda = b.lda_a; t.tstride = tsA;
+    t.act = b.actA; t.lda = b.lda_a;
     t.R = R; t.pos0 = pos0; t.H = H; t.Hkv = Hkv; t.max_ctx = c.max_ctx;
     t.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
     e = hd == 128 ? launch_pattn_t<128>(m, t) : launch_pattn_t<64>(m, t);
     if (e != hipSuccess) return e;
 
     PGemmArgs o{};
-    o.act = b.actA; o.lda = b.lda_a; o.tstride = tsA; o.R = R;
+    o.act = b.actA; o.lda = b.lda_a; o.R = R;
     o.w0 = L.wo; o.s0 = (const uint16_t*)L.so;
     o.N = d; o.K = H * hd; o.out = b.x; o.ldo = d;
-    o.act_next = b.actN; o.lda_next = d; o.tstride_next = tsN;
+    o.act_next = b.actN; o.lda_next = d;
     o.g_next = (const uint16_t*)L.ffn_norm; o.ss_out = b.ss; o.nss = nss;
     if ((e = launch_pgemm<PE_RESID>(m, o, (d + kUnit - 1) / kUnit)) != hipSuccess) return e;
 
     PGemmArgs gu{};
-    gu.act = b.actN; gu.lda = d; gu.tstride = tsN; gu.R = R;
+    gu.act = b.actN; gu.lda = d; gu.R = R;
     gu.ss_in = b.ss; gu.nss = nss; gu.eps = c.rms_eps;
     gu.w0 = L.w_gate; gu.w1 = L.w_up;
     gu.s0 = (const uint16_t*)L.s_gate; gu.s1 = (const uint16_t*)L.s_up;
     gu.N = F; gu.K = d;
-    gu.act_out = b.actB; gu.lda_out = b.lda_b; gu.tstride_out = tsB;
+    gu.act_out = b.actB; gu.lda_out = b.lda_b;
     if ((e = launch_pgemm<PE_SWIGLU>(m, gu, (F + 63) / 64)) != hipSuccess) return e;
 
     PGemmArgs dn{};
-    dn.act = b.actB; dn.lda = b.lda_b; dn.tstride = tsB; dn.R = R;
+    dn.act = b.actB; dn.lda = b.lda_b; dn.R = R;
     dn.w0 = L.w_down; dn.s0 = (const uint16_t*)L.s_down;
     dn.N = d; dn.K = F; dn.out = b.x; dn.ldo = d;
     if (!last) {
-      dn.act_next = b.actA; dn.lda_next = b.lda_a; dn.tstride_next = tsA;
+      dn.act_next = b.actA; dn.lda_next = b.lda_a;
       dn.g_next = (const uint16_t*)m.layers[(size_t)l + 1].attn_norm;
       dn.ss_out = b.ss; dn.nss = nss;
     }
