@@ -456,13 +456,18 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
     // read past the caches); the last slice to arrive adds them in slice
     // order, so the sum is the same whatever the arrival order
     // (element-major, so that each store and load instruction of a wave
-    // covers 256 contiguous bytes)
+    // covers 256 contiguous bytes).  Lanes of prompt rows past R move
+    // nothing: at a short prompt most of the tile's rows are (the last
+    // slice's reads of 8 partial tiles were half of a 23-row O product).
     const int tile = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+    const bool row_live = r0 + wr * 32 + rl < a.R;
     float* mine = a.fix + ((size_t)tile * a.ks + kz) * 32 * kGT + tid;
+    if (row_live) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      st_agent(mine + v * kGT, ylo[v]);
-      st_agent(mine + (16 + v) * kGT, yhi[v]);
+      for (int v = 0; v < 16; ++v) {
+        st_agent(mine + v * kGT, ylo[v]);
+        st_agent(mine + (16 + v) * kGT, yhi[v]);
+      }
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -473,7 +478,7 @@ __global__ __launch_bounds__(PTile<WN>::GT) void k_pgemm(PGemmArgs a) {
     if (tid == 0) atomic_store_agent(a.tcnt + tile, 0);  // ready for the next product
 #pragma unroll
     for (int v = 0; v < 16; ++v) ylo[v] = yhi[v] = 0.f;
-    for (int k = 0; k < a.ks; ++k) {
+    for (int k = 0; k < (row_live ? a.ks : 0); ++k) {
       const float* pk = a.fix + ((size_t)tile * a.ks + k) * 32 * kGT + tid;
       float plo[16], phi[16];
 #pragma unroll
