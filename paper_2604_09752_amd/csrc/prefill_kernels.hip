@@ -16,9 +16,9 @@
 //
 // Precision.  Activations stay fp32 between kernels.  The GEMMs run on MFMA
 // (v_mfma_f32_32x32x16_bf16) with every activation split exactly into three
-// bf16 terms as it is staged in LDS, a = t0 + t1 + t2 + r with |r| <= 2^-27 |a|, so the products
-// keep fp32 accuracy (two terms leave 2^-18, which measurably loosens the
-// cache rows of deeper layers).  Weights are exact in bf16 (int8 weights
+// bf16 terms as it is staged in LDS (a = t0 + t1 + t2), so the products keep
+// fp32 accuracy (two terms leave 2^-18, which measurably loosens the cache
+// rows of deeper layers).  Weights are exact in bf16 (int8 weights
 // convert exactly; their fp16 per-output-channel scale applies in the
 // epilogue).  Attention splits the queries and the softmax weights into
 // three terms as well.
@@ -1024,9 +1024,9 @@ hipError_t aio_launch_prefill_chunk(const aio_model& m, const PfBuffers& b, int 
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int nss = d / 64;
   hipError_t e;
-  // layer 0's input rows: the embeddings, with the split of x g and the
-  // sums of squares for its attention norm; every later norm input comes
-  // from the residual product before it
+  // layer 0's input rows: the embeddings, with x g and the sums of squares
+  // for its attention norm; every later norm input comes from the residual
+  // product before it
   if ((e = launch_pnorm(m, b, R, (const uint16_t*)m.embed, m.layers[0].attn_norm)) != hipSuccess)
     return e;
   for (int l = 0; l < c.n_layers; ++l) {
