@@ -264,6 +264,21 @@ struct GPhase {
 template <int WFMT>
 constexpr int epv() { return WFMT == AIO_WFMT_BF16 ? 8 : 16; }
 
+// Lanes that share one weight row in a load: the whole wave for bf16; a half
+// wave for int8, whose two halves take two rows.  A wave's K-slice of 4096
+// int8 inputs is 32 vectors of 16: spread over the wave it would leave half
+// the lanes multiplying zeros (the int8 loops were bound by that waste),
+// and 8-byte loads instead would double the load instructions per byte.
+template <int WFMT>
+constexpr int lpr() { return WFMT == AIO_WFMT_INT8 ? AIO_WAVE / 2 : AIO_WAVE; }
+
+// The K-slice vector of a lane's load v.
+template <int WFMT>
+AIO_DEV int lane_vec(int v, int lane) {
+  if constexpr (lpr<WFMT>() == AIO_WAVE) return v * AIO_WAVE + lane;
+  else return v * lpr<WFMT>() + (lane & (lpr<WFMT>() - 1));
+}
+
 // Units of a matrix phase: QKV unit u = rotation pairs 2u, 2u+1 (rows lo
 // and hi of each); GU unit = row n of gate and of up; else one row.
 template <int KIND>
@@ -377,17 +392,30 @@ AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[k
   constexpr int RPU = rpu_of<KIND>();
   constexpr int UB = kNLD / (RPU * VPL);
   static_assert(UB >= 1, "a batch must hold at least one unit");
+  constexpr bool HALF = lpr<WFMT>() < AIO_WAVE;
   const int lane = T.lane, wave = T.wave;
   const int ulast = P.nu - 1;
 #pragma unroll
   for (int j = 0; j < UB * RPU * VPL; ++j) {
     const int ul = j / (RPU * VPL), r = (j / VPL) % RPU, v = j % VPL;
-    const int u = P.u0 + batch * UB + ul;
-    const int vi = v * AIO_WAVE + lane;
-    const bool ok = slot_ok(P, u, vi);
-    const char* rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, r));
-    const uint4* p = (const uint4*)rb + (size_t)wave * P.nvw + (ok ? vi : 0);
-    buf[j] = ldg_stream(p);
+    if constexpr (HALF) {
+      // units 2 ul and 2 ul + 1 of the batch in the lower and upper half
+      const int vi = lane_vec<WFMT>(v, lane);
+      const int ua = P.u0 + batch * 2 * UB + 2 * ul, ub = ua + 1;
+      const char* r0 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ua < ulast ? ua : ulast, r));
+      const char* r1 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ub < ulast ? ub : ulast, r));
+      const bool hi = lane >= AIO_WAVE / 2;
+      const bool ok = slot_ok(P, hi ? ub : ua, vi);
+      const uint4* p = (const uint4*)(hi ? r1 : r0) + (size_t)wave * P.nvw + (ok ? vi : 0);
+      buf[j] = ldg_stream(p);
+    } else {
+      const int u = P.u0 + batch * UB + ul;
+      const int vi = v * AIO_WAVE + lane;
+      const bool ok = slot_ok(P, u, vi);
+      const char* rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, r));
+      const uint4* p = (const uint4*)rb + (size_t)wave * P.nvw + (ok ? vi : 0);
+      buf[j] = ldg_stream(p);
+    }
   }
 }
 
@@ -424,6 +452,21 @@ AIO_DEV float reduce_rows(float (&v)[N], int lane) {
   return s;
 }
 
+// The same over each half wave (lanes 0-31 and 32-63 separately): lane l
+// then holds value ((l >> (5 - log2 N)) & (N - 1)) of half l / 32.
+template <int N>
+AIO_DEV float reduce_rows_half(float (&v)[N], int lane) {
+  static_assert(N == 2 || N == 4 || N == 8, "reduce_rows_half takes 2, 4 or 8 values");
+  constexpr int LOG = log2_of<N>();
+  halve<16, N / 2>(v, lane);
+  if constexpr (N >= 4) halve<8, N / 4>(v, lane);
+  if constexpr (N >= 8) halve<4, 1>(v, lane);
+  float s = v[0];
+#pragma unroll
+  for (int off = 16 >> LOG; off >= 1; off >>= 1) s += __shfl_xor(s, off, AIO_WAVE);
+  return s;
+}
+
 // Multiply-accumulate one batch and leave each wave's row partials in LDS
 // red[(local unit * RPU + r) * kW + wave].  Slots are not masked here: a
 // lane past the end of its K-slice holds h = 0 (input_finish) and reads a
@@ -453,13 +496,23 @@ AIO_DEV void compute(const GPhase& P, int batch, const uint4 (&buf)[kNLD],
       t = dot4_i8(w.w, make_float4(h[v][12], h[v][13], h[v][14], h[v][15]), t);
     }
   }
-  const float s = reduce_rows<kNLD>(acc, lane);
   constexpr int LOG = log2_of<kNLD>();
-  const int idx = (lane >> (6 - LOG)) & (kNLD - 1);
-  if ((lane & ((AIO_WAVE >> LOG) - 1)) == 0 && idx < UB * RPU) {
-    const int ul = idx / RPU, r = idx % RPU;
-    const int lu = batch * UB + ul;
-    if (P.u0 + lu < P.u1) red[(lu * RPU + r) * kW + wave] = s;
+  if constexpr (lpr<WFMT>() < AIO_WAVE) {
+    const float s = reduce_rows_half<kNLD>(acc, lane);
+    const int idx = (lane >> (5 - LOG)) & (kNLD - 1), hf = lane >> 5;
+    if ((lane & ((AIO_WAVE / 2 >> LOG) - 1)) == 0 && idx < UB * RPU) {
+      const int ul = idx / RPU, r = idx % RPU;
+      const int lu = batch * 2 * UB + 2 * ul + hf;
+      if (P.u0 + lu < P.u1) red[(lu * RPU + r) * kW + wave] = s;
+    }
+  } else {
+    const float s = reduce_rows<kNLD>(acc, lane);
+    const int idx = (lane >> (6 - LOG)) & (kNLD - 1);
+    if ((lane & ((AIO_WAVE >> LOG) - 1)) == 0 && idx < UB * RPU) {
+      const int ul = idx / RPU, r = idx % RPU;
+      const int lu = batch * UB + ul;
+      if (P.u0 + lu < P.u1) red[(lu * RPU + r) * kW + wave] = s;
+    }
   }
 }
 
@@ -493,7 +546,7 @@ AIO_DEV void input_issue(const MegaArgs& a, const GPhase& P, int layer, Input<WF
     const uint16_t* g = KIND == K_QKV ? L->attn_norm : (KIND == K_GU ? L->ffn_norm : a.final_norm);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      const int vi = v * AIO_WAVE + lane;
+      const int vi = lane_vec<WFMT>(v, lane);
       const int e0 = (wave * P.nvw + (vi < P.nvw ? vi : 0)) * E;
 #pragma unroll
       for (int j = 0; j < NG; ++j) I.gw[v][j] = ldg16(g + e0 + 8 * j);
@@ -503,7 +556,7 @@ AIO_DEV void input_issue(const MegaArgs& a, const GPhase& P, int layer, Input<WF
   const unsigned* src = KIND == K_O ? a.o : (KIND == K_DOWN ? a.m : (KIND == K_GU ? a.xa : a.xb));
 #pragma unroll
   for (int v = 0; v < VPL; ++v) {
-    const int vi = v * AIO_WAVE + lane;
+    const int vi = lane_vec<WFMT>(v, lane);
     const bool ok = vi < P.nvw;
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
@@ -533,7 +586,7 @@ AIO_DEV void input_finish(const MegaArgs& a, const GPhase& P, int layer, int tok
     const uint16_t* er = a.embed + (size_t)token * a.d;
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      const int vi = v * AIO_WAVE + lane;
+      const int vi = lane_vec<WFMT>(v, lane);
       const bool ok = vi < P.nvw;
       const int e0 = (wave * P.nvw + (ok ? vi : 0)) * E;
 #pragma unroll
@@ -570,6 +623,7 @@ AIO_DEV void input_finish(const MegaArgs& a, const GPhase& P, int layer, int tok
 #pragma unroll
       for (int i = 0; i < E; ++i) ss = fmaf(h[v][i], h[v][i], ss);
     }
+    if (lpr<WFMT>() < AIO_WAVE && lane >= AIO_WAVE / 2) ss = 0.f;  // the halves hold the same slice
     ss = wave_sum(ss);
     if (lane == 0) ss8[wave] = ss;
 #pragma unroll
@@ -825,7 +879,8 @@ AIO_DEV void gemv_phase(const MegaArgs& a, int layer, int pos, int token, Bufs& 
   // previous phase's partials in its epilogue
   float* red = lds + (k & 1u) * (unsigned)a.red_words;
   float* ss8 = sm.ss8[k & 1u];
-  constexpr int UB = kNLD / (RPU * VPL);
+  // units per batch (two halves of a wave take two units each slot for int8)
+  constexpr int UB = kNLD / (RPU * VPL) * (AIO_WAVE / lpr<WFMT>());
   const GPhase P = make_phase<WFMT, KIND>(a, layer);
   const int nb = (P.u1 - P.u0 + UB - 1) / UB;
   const unsigned slot = KIND == K_LM ? 0u : k;  // timing slot
@@ -1317,10 +1372,12 @@ hipError_t launch_g(const MegaArgs& a, int blocks, size_t lds, hipStream_t s, in
 }  // namespace
 
 int aio_step_kernel_vpl(const aio_config& c, int K) {
-  const int epv_ = c.wfmt == AIO_WFMT_BF16 ? 8 : 16;
+  const bool i8 = c.wfmt == AIO_WFMT_INT8;
+  const int epv_ = i8 ? epv<AIO_WFMT_INT8>() : epv<AIO_WFMT_BF16>();
+  const int lpr_ = i8 ? lpr<AIO_WFMT_INT8>() : lpr<AIO_WFMT_BF16>();
   if (K % (kW * epv_)) return 0;
   const int nvw = K / (kW * epv_);
-  return (nvw + AIO_WAVE - 1) / AIO_WAVE;
+  return (nvw + lpr_ - 1) / lpr_;
 }
 
 bool aio_step_kernel_supports(const aio_config& c) {
