@@ -115,7 +115,13 @@ WsLayout aio_ws_layout(const aio_config& c) {
   L.vacnt = off; off = align256(off + (size_t)c.n_heads * 4);
   L.amax = off; off = align256(off + MV * 4);
   L.sync = off; off = align256(off + (size_t)kSyncWords * 4);
-  L.mega_splits = AIO_STEP_MAX_BLOCKS / c.n_kv_heads;
+  // split-KV partitions per kv head in the step kernel: one per workgroup,
+  // but at most 16.  With fewer kv heads the splits get short and the merge
+  // of their partials long: the 1B (8 kv heads) at 2K positions, 32 splits
+  // of 64 keys, 1204 tokens/s; 16 splits 1232; 8 splits 1197; 4 splits 1113.
+  // (Fixed per model: a partial slot's previous contents must always come
+  // from the previous layer, which its version tag tells apart.)
+  L.mega_splits = std::min(AIO_STEP_MAX_BLOCKS / c.n_kv_heads, 16);
   if (L.mega_splits < 1) L.mega_splits = 1;
   L.mega_xa = off; off = align256(off + d * 4);
   L.mega_xb = off; off = align256(off + d * 4);
