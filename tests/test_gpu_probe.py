@@ -40,10 +40,16 @@ CASES = {
     "split_k": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128), 0, 23),
     "split_k_int8": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
                           wfmt="int8"), 0, 70),
-    # 1100 prompt rows (18 tiles of 64): 256-row weight tiles of 8 waves, K
-    # still split in two for QKV and O
+    # 1100 prompt rows (18 tiles of 64): 256-row weight tiles of 8 waves; K
+    # split in two for O and down, while QKV (216 workgroups) and gate/up
+    # (576) run unsplit in the XCD-renumbered order, whose last band holds 2
+    # of the 18 row tiles; attention gives each XCD one of the 8 heads
     "wide_tiles": (dict(d_model=1024, ffn_dim=4096, n_heads=8, n_kv_heads=8, head_dim=128,
                         prompt_len=1100), 0, 1100),
+    # 16 query heads on 8 kv heads (G = 2), hd 64: attention gives each XCD
+    # two heads, which share one kv head
+    "xcd_heads_gqa": (dict(d_model=1024, ffn_dim=2048, n_heads=16, n_kv_heads=8, head_dim=64,
+                           prompt_len=300), 0, 300),
 }
 
 
