@@ -318,8 +318,9 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
  * aio_decode_step calls up to rounding.  A prompt of at most max_verify
  * tokens goes through the verify forward instead (the same kernels as
  * aio_verify; no scratch beyond the workspace).  The scratch
- * (4 (1 + d + H hd + max(d, H hd) + F) bytes per row, for up to 2048 rows) is allocated by
- * the library on the first call that needs more and kept until
+ * (4 (1 + 2 d + H hd + max(d, H hd) + F) + d / 16 bytes per row, for up to
+ * 2048 rows) is allocated by the library on the first call that needs more
+ * and kept until
  * aio_model_free, so such a call synchronises once.  Asynchronous
  * otherwise, like aio_verify.
  * AIO_ERANGE: n < 1, pos < 0, pos + n > max_ctx or a token outside
