@@ -402,8 +402,21 @@ AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[k
       // units 2 ul and 2 ul + 1 of the batch in the lower and upper half
       const int vi = lane_vec<WFMT>(v, lane);
       const int ua = P.u0 + batch * 2 * UB + 2 * ul, ub = ua + 1;
-      const char* r0 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ua < ulast ? ua : ulast, r));
-      const char* r1 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ub < ulast ? ub : ulast, r));
+      const char* r0;
+      const char* r1;
+      if constexpr (KIND == K_QKV) {
+        // a QKV unit's four rows lie at virtual rows 0, 1, hd/2, hd/2 + 1
+        // of its first, in one head and so in one matrix: one row base per
+        // unit (recomputed for every row, the scalar address arithmetic
+        // took as many instructions as the products)
+        static_assert(WFMT == AIO_WFMT_INT8, "half-wave rows are int8 (one byte per weight)");
+        const size_t ro = (size_t)((r & 1) + (r >> 1) * (HD / 2)) * (size_t)P.K;
+        r0 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ua < ulast ? ua : ulast, 0)) + ro;
+        r1 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ub < ulast ? ub : ulast, 0)) + ro;
+      } else {
+        r0 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ua < ulast ? ua : ulast, r));
+        r1 = wave_uniform(row_base<WFMT, KIND, HD>(a, P, ub < ulast ? ub : ulast, r));
+      }
       const bool hi = lane >= AIO_WAVE / 2;
       const bool ok = slot_ok(P, hi ? ub : ua, vi);
       const uint4* p = (const uint4*)(hi ? r1 : r0) + (size_t)wave * P.nvw + (ok ? vi : 0);
@@ -412,7 +425,14 @@ AIO_DEV void issue(const MegaArgs& a, const GPhase& P, int batch, uint4 (&buf)[k
       const int u = P.u0 + batch * UB + ul;
       const int vi = v * AIO_WAVE + lane;
       const bool ok = slot_ok(P, u, vi);
-      const char* rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, r));
+      const char* rb;
+      if constexpr (KIND == K_QKV) {  // one row base per unit, as above
+        constexpr size_t wb = WFMT == AIO_WFMT_BF16 ? 2 : 1;
+        const size_t ro = (size_t)((r & 1) + (r >> 1) * (HD / 2)) * (size_t)P.K * wb;
+        rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, 0)) + ro;
+      } else {
+        rb = wave_uniform(row_base<WFMT, KIND, HD>(a, P, u < ulast ? u : ulast, r));
+      }
       const uint4* p = (const uint4*)rb + (size_t)wave * P.nvw + (ok ? vi : 0);
       buf[j] = ldg_stream(p);
     }
