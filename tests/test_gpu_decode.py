@@ -59,6 +59,11 @@ VARIANTS = {
     "int8": dict(wfmt="int8"),
     "int8_gqa2_ragged": dict(wfmt="int8", n_heads=4, n_kv_heads=2, d_model=320, ffn_dim=192,
                              vocab=1000),
+    # int8, FFN 6144: the step kernel's down rows take two 16-byte vectors per
+    # half-wave lane (48 per wave's slice), and a batch of 8 down units holds
+    # 2 of a workgroup's rows and 6 past them
+    "int8_wide_ffn": dict(wfmt="int8", d_model=512, ffn_dim=6144, n_heads=8, n_kv_heads=8,
+                          head_dim=64),
 }
 
 
