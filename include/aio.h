@@ -315,9 +315,10 @@ int aio_pld_generate(aio_model* m, const int32_t* history, int32_t pos, int32_t 
  * rows per pass over the weights) with causal attention, writes every
  * token's K/V in every layer, and writes the logits after the last token,
  * fp32 [vocab], to logits_dev (16-byte aligned).  The result equals n
- * aio_decode_step calls up to rounding.  A prompt of at most max_verify
- * tokens goes through the verify forward instead (the same kernels as
- * aio_verify; no scratch beyond the workspace).  The scratch
+ * aio_decode_step calls up to rounding.  A single token is one decode step
+ * (the kernels of aio_decode_step), and a prompt of 2 to max_verify tokens
+ * goes through the verify forward (the kernels of aio_verify); neither takes
+ * scratch beyond the workspace.  The scratch
  * (4 (1 + 2 d + H hd + max(d, H hd) + F) + d / 16 bytes per row, for up to
  * 2048 rows) is allocated by the library on the first call that needs more
  * and kept until

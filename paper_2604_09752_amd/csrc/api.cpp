@@ -684,12 +684,19 @@ static hipError_t enqueue_prefill(aio_model* m, const PfBuffers& b, const int32_
 }
 
 // A prompt of at most max_verify tokens goes through the verify forward
-// (skinny products over the weights once): at the 1B, 10 tokens take 1.6
+// (skinny products over the weights once): at the 1B, 10 tokens take 1.5
 // against 3.7 ms in prompt-length products, whose tiles are 64 rows.
 static bool prefill_as_verify(const aio_model* m, int32_t n) { return n <= m->cfg.max_verify; }
 
+// A single token is one decode step (the persistent kernel: 0.80 against
+// 1.25 ms for the 1B in the verify forward).
 static hipError_t enqueue_prefill_as_verify(aio_model* m, const int32_t* tokens, int32_t n,
                                             int32_t pos, float* logits_dev) {
+  if (n == 1) {
+    hipError_t e = aio_launch_set_state(*m, tokens[0], pos);
+    if (e == hipSuccess) e = enqueue_step_body(m, logits_dev);
+    return e;
+  }
   hipError_t e = aio_launch_set_rows(*m, tokens, n, pos);
   if (e == hipSuccess) e = aio_launch_verify(*m, n, pos, logits_dev, true);
   return e;
